@@ -1,0 +1,15 @@
+"""fp64 CPU oracle for chunk-wise causal attention.
+
+TEST INFRASTRUCTURE ONLY: used by tests/, the smoke check and the benchmark's
+CPU-baseline leg.  The HIP library never imports, links or calls it."""
+from .chunk_attention import (  # noqa: F401
+    attention,
+    brute_force,
+    count_visible_pairs,
+    frame_mask,
+    key_chunks,
+    kv_cache_append,
+    query_chunks,
+    softmax_weights,
+    visibility_mask,
+)

@@ -1,0 +1,217 @@
+"""Plain fp64 CPU oracle for chunk-wise causal self-attention (FastVR, Sec. 3.1).
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or link
+this module: only the test suite, the smoke check and the benchmark's
+``cpu_baseline`` leg use it.  It shares no code with the HIP library.
+
+What is computed (Sec. 3.1, Eq. 1 and the paragraph after it):
+
+* Latent tokens are flattened frame-major, so a chunk of ``k`` latent frames is
+  a contiguous token range of ``chunk_len = k * tokens_per_frame`` tokens and
+  the frame-level mask of Eq. 1 becomes a token-level mask on
+  ``floor(token / chunk_len)``.
+* Query row ``i`` belongs to chunk ``cq(i) = q_chunk_offset + i // chunk_len``,
+  key row ``j`` to chunk ``ck(j) = j // chunk_len``.  Key ``j`` is visible to
+  query ``i`` when ``0 <= cq(i) - ck(j) <= W``.  Eq. 1 is ``W = 1`` ("itself and
+  its immediate predecessor"); ``window_chunks = -1`` means no upper bound (an
+  unbounded causal prefix of chunks).  Inside a chunk attention is
+  bidirectional.
+* ``LSE_i = ln sum_{j visible} exp(scale * q_i . k_j)`` and
+  ``O_i = sum_{j visible} exp(scale * q_i . k_j - LSE_i) v_j``.
+* The parallel (training) form over the whole sequence and the streaming form
+  (one query chunk against a KV cache, ``q_chunk_offset`` = its chunk index)
+  are the same function (Sec. 3.1, last paragraph).
+
+Everything is evaluated in float64 from the given inputs (bf16 inputs are
+widened exactly).  ``scale`` is used exactly as passed; callers that model an
+fp32 interface pass the fp32-rounded value.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+# ---------------------------------------------------------------------------
+# Mask (Eq. 1, generalised to a window of W previous chunks)
+# ---------------------------------------------------------------------------
+
+def query_chunks(nq: int, chunk_len: int, q_chunk_offset: int = 0) -> np.ndarray:
+    """Chunk index of every query row: q_chunk_offset + i // chunk_len."""
+    return q_chunk_offset + np.arange(nq, dtype=np.int64) // chunk_len
+
+
+def key_chunks(nkv: int, chunk_len: int) -> np.ndarray:
+    """Chunk index of every key row: j // chunk_len."""
+    return np.arange(nkv, dtype=np.int64) // chunk_len
+
+
+def visibility_mask(nq: int, nkv: int, chunk_len: int, q_chunk_offset: int = 0,
+                    window_chunks: int = -1, rows=None) -> np.ndarray:
+    """Explicit boolean mask [len(rows), nkv]: True where key j is visible to query i.
+
+    Eq. 1 with the chunk difference allowed in {0..W} (W = -1: any non-negative
+    difference)."""
+    cq = query_chunks(nq, chunk_len, q_chunk_offset)
+    if rows is not None:
+        cq = cq[np.asarray(rows, dtype=np.int64)]
+    ck = key_chunks(nkv, chunk_len)
+    diff = cq[:, None] - ck[None, :]
+    vis = diff >= 0
+    if window_chunks >= 0:
+        vis &= diff <= window_chunks
+    return vis
+
+
+def frame_mask(num_frames: int, frames_per_chunk: int, window_chunks: int = 1) -> np.ndarray:
+    """Eq. 1 at the level of latent frames: M[i, j] = 1 iff floor(i/k) - floor(j/k)
+    lies in {0..W} (the paper's W is 1)."""
+    f = np.arange(num_frames, dtype=np.int64) // frames_per_chunk
+    diff = f[:, None] - f[None, :]
+    m = diff >= 0
+    if window_chunks >= 0:
+        m &= diff <= window_chunks
+    return m
+
+
+def count_visible_pairs(nq: int, nkv: int, chunk_len: int, q_chunk_offset: int = 0,
+                        window_chunks: int = -1, block: int = 4096) -> int:
+    """Number of visible (query, key) pairs, counted from the explicit mask."""
+    total = 0
+    for r0 in range(0, nq, block):
+        rows = np.arange(r0, min(nq, r0 + block))
+        total += int(visibility_mask(nq, nkv, chunk_len, q_chunk_offset,
+                                     window_chunks, rows=rows).sum())
+    return total
+
+
+# ---------------------------------------------------------------------------
+# Masked softmax attention, straight from the definition
+# ---------------------------------------------------------------------------
+
+def _as_f64(x) -> np.ndarray:
+    if hasattr(x, "detach"):  # a torch tensor; bf16 has no numpy dtype
+        import torch
+        x = x.detach().to("cpu", torch.float64).numpy()
+    return np.asarray(x, dtype=np.float64)
+
+
+def attention(q, k, v, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
+              scale: float | None = None, rows=None, block: int = 512):
+    """Chunk-causal attention in fp64.
+
+    q: [B, Nq, H, d]; k, v: [B, Nkv, H, d] (numpy arrays or CPU torch tensors).
+    rows: optional 1-D array of query-row indices to evaluate (all rows if None).
+    Returns (o [B, R, H, d] float64, lse [B, H, R] float64) with R = number of rows.
+
+    Per (b, h) and block of query rows: S = scale * Q K^T, S = -inf where the mask
+    hides the key, m = rowmax S, P = exp(S - m), l = rowsum P, O = P V / l,
+    LSE = m + ln l."""
+    q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
+    B, nq, H, d = q.shape
+    nkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    scale = float(scale)
+    rows = np.arange(nq, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    R = rows.shape[0]
+    o = np.zeros((B, R, H, d), dtype=np.float64)
+    lse = np.zeros((B, H, R), dtype=np.float64)
+    for r0 in range(0, R, block):
+        rr = rows[r0:r0 + block]
+        vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows=rr)
+        if not vis.any(axis=1).all():
+            raise ValueError("a query row has no visible key")
+        for b in range(B):
+            for h in range(H):
+                s = scale * (q[b, rr, h, :] @ k[b, :, h, :].T)
+                s = np.where(vis, s, -np.inf)
+                m = s.max(axis=1, keepdims=True)
+                p = np.exp(s - m)
+                l = p.sum(axis=1, keepdims=True)
+                o[b, r0:r0 + len(rr), h, :] = (p @ v[b, :, h, :]) / l
+                lse[b, h, r0:r0 + len(rr)] = (m + np.log(l))[:, 0]
+    return o, lse
+
+
+def softmax_weights(q, k, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
+                    scale: float | None = None, b: int = 0, h: int = 0) -> np.ndarray:
+    """The attention weights P [Nq, Nkv] of one (b, h), masked entries exactly 0.
+    For small inputs only (exposes the normalisation invariant)."""
+    q = _as_f64(q)
+    k = _as_f64(k)
+    nq, d = q.shape[1], q.shape[3]
+    nkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks)
+    s = np.where(vis, float(scale) * (q[b, :, h, :] @ k[b, :, h, :].T), -np.inf)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    return p / p.sum(axis=1, keepdims=True)
+
+
+# ---------------------------------------------------------------------------
+# Brute force at the level of latent frames (Eq. 1 exactly as printed)
+# ---------------------------------------------------------------------------
+
+def brute_force(q, k, v, tokens_per_frame: int, frames_per_chunk: int,
+                q_chunk_offset: int = 0, window_chunks: int = 1,
+                scale: float | None = None):
+    """Pure-Python loops, for tiny inputs only.
+
+    The token n lies in latent frame n // tokens_per_frame; frames are grouped in
+    chunks of ``frames_per_chunk`` (k of Eq. 1).  Query row i lies in frame
+    q_chunk_offset * frames_per_chunk + i // tokens_per_frame.  Eq. 1's test
+    floor(fi/k) - floor(fj/k) in {0..W} decides visibility.  Dot products and sums
+    use math.fsum; the softmax is evaluated with the row maximum subtracted."""
+    q = _as_f64(q)
+    k = _as_f64(k)
+    v = _as_f64(v)
+    B, nq, H, d = q.shape
+    nkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    o = np.zeros((B, nq, H, d))
+    lse = np.zeros((B, H, nq))
+    for b in range(B):
+        for h in range(H):
+            for i in range(nq):
+                fi = q_chunk_offset * frames_per_chunk + i // tokens_per_frame
+                ci = fi // frames_per_chunk
+                vis_j = []
+                for j in range(nkv):
+                    cj = (j // tokens_per_frame) // frames_per_chunk
+                    delta = ci - cj
+                    if delta >= 0 and (window_chunks < 0 or delta <= window_chunks):
+                        vis_j.append(j)
+                if not vis_j:
+                    raise ValueError("a query row has no visible key")
+                scores = [scale * math.fsum(q[b, i, h, x] * k[b, j, h, x] for x in range(d))
+                          for j in vis_j]
+                mx = max(scores)
+                w = [math.exp(s - mx) for s in scores]
+                tot = math.fsum(w)
+                lse[b, h, i] = mx + math.log(tot)
+                for x in range(d):
+                    o[b, i, h, x] = math.fsum(wj * v[b, j, h, x] for wj, j in zip(w, vis_j)) / tot
+    return o, lse
+
+
+# ---------------------------------------------------------------------------
+# KV cache append (streaming inference with KV caching, Sec. 3.1)
+# ---------------------------------------------------------------------------
+
+def kv_cache_append(k_cache, v_cache, k_new, v_new, cache_len: int):
+    """Return copies of the caches ([B, capacity, H, d]) with the new tokens
+    ([B, n_new, H, d]) written at token offset cache_len.  No eviction."""
+    kc = np.array(k_cache, copy=True)
+    vc = np.array(v_cache, copy=True)
+    n_new = np.shape(k_new)[1]
+    if cache_len + n_new > kc.shape[1]:
+        raise ValueError("append would overflow the cache")
+    kc[:, cache_len:cache_len + n_new] = k_new
+    vc[:, cache_len:cache_len + n_new] = v_new
+    return kc, vc

@@ -1,0 +1,393 @@
+"""Pins for the fp64 oracle (CPU only).
+
+The paper prints no worked numeric example, so the oracle is pinned by a
+hand-derived example (tests/golden/hand_example.csv), by brute force on the
+frame-level mask of Eq. 1, by a library attention routine where the mask is
+trivial, by closed forms, and by the invariants the method states (Sec. 3.1):
+causality, streaming == parallel, bidirectional attention inside a chunk."""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import chunk_attention as oc
+from paper_2609_36757_amd import metrics
+from paper_2609_36757_amd.workloads import make_qkv
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_example.csv")
+
+
+def _f64(*ts):
+    return [t.to(torch.float64).numpy() for t in ts]
+
+
+def _rand(B, nq, nkv, H, d, seed):
+    return _f64(*make_qkv(B, nq, nkv, H, d, seed))
+
+
+# ---------------------------------------------------------------------------
+# hand-derived worked example
+# ---------------------------------------------------------------------------
+
+def _hand_inputs(nq, q_off):
+    n = 6
+    q = np.ones((1, nq, 1, 1))
+    k = np.log(np.arange(1, n + 1, dtype=np.float64)).reshape(1, n, 1, 1)
+    v = np.arange(n, dtype=np.float64).reshape(1, n, 1, 1)
+    return q, k, v
+
+
+def _golden_rows():
+    rows = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            w, off, nq, row, onum, oden, larg = (int(x) for x in line.split(","))
+            rows.append((w, off, nq, row, onum / oden, math.log(larg)))
+    assert len(rows) >= 10
+    return rows
+
+
+def check_hand_example(attn=oracle.attention):
+    for w, off, nq, row, o_exp, lse_exp in _golden_rows():
+        q, k, v = _hand_inputs(nq, off)
+        o, lse = attn(q, k, v, chunk_len=2, q_chunk_offset=off, window_chunks=w, scale=1.0)
+        assert abs(o[0, row, 0, 0] - o_exp) < 1e-12, (w, off, row, o[0, row, 0, 0], o_exp)
+        assert abs(lse[0, 0, row] - lse_exp) < 1e-12, (w, off, row, lse[0, 0, row], lse_exp)
+
+
+def test_hand_example():
+    check_hand_example()
+
+
+def test_hand_example_brute_force():
+    for w, off, nq, row, o_exp, lse_exp in _golden_rows():
+        q, k, v = _hand_inputs(nq, off)
+        o, lse = oracle.brute_force(q, k, v, tokens_per_frame=1, frames_per_chunk=2,
+                                    q_chunk_offset=off, window_chunks=w, scale=1.0)
+        assert abs(o[0, row, 0, 0] - o_exp) < 1e-12
+        assert abs(lse[0, 0, row] - lse_exp) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# mask semantics
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("hw,kf,T,W", [(1, 3, 10, 1), (4, 2, 7, 1), (3, 3, 9, 2), (5, 1, 6, 0),
+                                       (2, 2, 8, -1)])
+def test_token_mask_is_frame_mask(hw, kf, T, W):
+    """Frame-major flattening: floor(floor(n/hw)/k) == floor(n/(k hw)), so the
+    token mask with chunk_len = k*hw is Eq. 1's frame mask expanded per token."""
+    fm = oracle.frame_mask(T, kf, W)
+    tm = oracle.visibility_mask(T * hw, T * hw, kf * hw, 0, W)
+    np.testing.assert_array_equal(tm, np.kron(fm, np.ones((hw, hw), dtype=bool)))
+
+
+def test_frame_mask_eq1_literal():
+    # Eq. 1 with k = 3, T = 9: chunk 1 (frames 3..5) sees frames 0..5, chunk 2 sees 3..8.
+    m = oracle.frame_mask(9, 3, 1)
+    assert m[4].tolist() == [True] * 6 + [False] * 3
+    assert m[8].tolist() == [False] * 3 + [True] * 6
+    assert m[0].tolist() == [True] * 3 + [False] * 6
+
+
+@pytest.mark.parametrize("nq,nkv,L,off,W", [
+    (37, 37, 5, 0, -1), (37, 37, 5, 0, 0), (37, 37, 5, 0, 1), (37, 37, 5, 0, 2),
+    (11, 40, 7, 2, -1), (11, 40, 7, 2, 1), (9, 30, 4, 5, 2), (64, 64, 64, 0, -1),
+    (100, 230, 13, 7, 3), (1, 1, 1, 0, -1)])
+def test_visible_pair_count_closed_form(nq, nkv, L, off, W):
+    assert metrics.visible_pairs(nq, nkv, L, off, W) == oracle.count_visible_pairs(nq, nkv, L, off, W)
+
+
+def test_visible_pairs_workload_shapes():
+    # the 1080p sequence: chunk c sees (c+1) chunks -> L^2 * (1+2+3+4)
+    L = 16320
+    assert metrics.visible_pairs(4 * L, 4 * L, L) == L * L * 10
+    assert metrics.visible_pairs(L, 4 * L, L, q_chunk_offset=3) == 4 * L * L
+    # wide window: 8 full chunks + a half chunk, W = 2
+    n = 8 * L + L // 2
+    exp = L * L * (1 + 2 + 3 * 6) + (L // 2) * (2 * L + L // 2)
+    assert metrics.visible_pairs(n, n, L, 0, 2) == exp
+
+
+# ---------------------------------------------------------------------------
+# brute force on tiny inputs (Eq. 1 at the frame level, math.fsum loops)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("W", [-1, 0, 1, 2])
+@pytest.mark.parametrize("hw,kf,nframes,off,nq", [(2, 2, 7, 0, 14), (3, 1, 6, 0, 13),
+                                                   (1, 3, 11, 0, 11), (2, 2, 8, 1, 9),
+                                                   (3, 2, 9, 3, 6)])
+def test_oracle_matches_brute_force(W, hw, kf, nframes, off, nq):
+    nkv = hw * nframes
+    L = hw * kf
+    if off * L + nq > nkv:
+        nq = nkv - off * L
+    q, k, v = _rand(2, nq, nkv, 2, 8, seed=100 + W * 7 + hw * 3 + off)
+    o1, l1 = oracle.attention(q, k, v, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=0.3)
+    o2, l2 = oracle.brute_force(q, k, v, tokens_per_frame=hw, frames_per_chunk=kf,
+                                q_chunk_offset=off, window_chunks=W, scale=0.3)
+    np.testing.assert_allclose(o1, o2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(l1, l2, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# library routine where the mask is trivial
+# ---------------------------------------------------------------------------
+
+def _sdpa(q, k, v, scale):
+    """torch's scaled_dot_product_attention in fp64 on [n, d] per (b, h)."""
+    qt = torch.from_numpy(q).permute(0, 2, 1, 3)  # B H N d
+    kt = torch.from_numpy(k).permute(0, 2, 1, 3)
+    vt = torch.from_numpy(v).permute(0, 2, 1, 3)
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)
+    lse = torch.logsumexp(scale * (qt @ kt.transpose(-1, -2)), dim=-1)
+    return o.permute(0, 2, 1, 3).numpy(), lse.numpy()
+
+
+def test_one_chunk_equals_full_attention():
+    q, k, v = _rand(2, 50, 50, 3, 16, seed=7)
+    o, lse = oracle.attention(q, k, v, chunk_len=64, scale=0.25)
+    o2, lse2 = _sdpa(q, k, v, 0.25)
+    np.testing.assert_allclose(o, o2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lse2, rtol=0, atol=1e-12)
+
+
+def test_window_zero_is_blockwise_full_attention():
+    L, C = 6, 4
+    q, k, v = _rand(1, L * C, L * C, 2, 8, seed=8)
+    o, lse = oracle.attention(q, k, v, chunk_len=L, window_chunks=0, scale=0.4)
+    for c in range(C):
+        s = slice(c * L, (c + 1) * L)
+        o2, lse2 = _sdpa(q[:, s], k[:, s], v[:, s], 0.4)
+        np.testing.assert_allclose(o[:, s], o2, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse[:, :, s], lse2, rtol=0, atol=1e-12)
+
+
+def test_full_prefix_last_chunk_is_full_attention():
+    """With W = -1 the last chunk sees every key: plain attention over all keys."""
+    L, C = 5, 4
+    q, k, v = _rand(1, L * C, L * C, 2, 8, seed=9)
+    o, lse = oracle.attention(q, k, v, chunk_len=L, window_chunks=-1, scale=0.4)
+    s = slice((C - 1) * L, C * L)
+    o2, lse2 = _sdpa(q[:, s], k, v, 0.4)
+    np.testing.assert_allclose(o[:, s], o2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse[:, :, s], lse2, rtol=0, atol=1e-12)
+
+
+def test_large_window_equals_unbounded():
+    L, C = 4, 5
+    q, k, v = _rand(1, L * C - 2, L * C - 2, 2, 8, seed=10)
+    a = oracle.attention(q, k, v, chunk_len=L, window_chunks=C - 1, scale=0.5)
+    b = oracle.attention(q, k, v, chunk_len=L, window_chunks=-1, scale=0.5)
+    c = oracle.attention(q, k, v, chunk_len=L, window_chunks=C + 10, scale=0.5)
+    for x, y in ((a, b), (c, b)):
+        np.testing.assert_array_equal(x[0], y[0])
+        np.testing.assert_array_equal(x[1], y[1])
+
+
+# ---------------------------------------------------------------------------
+# closed forms
+# ---------------------------------------------------------------------------
+
+def _n_visible_closed(i, L, nkv, off, W):
+    c = off + i // L
+    lo = 0 if W < 0 else max(0, c - W) * L
+    hi = min((c + 1) * L, nkv)
+    return lo, hi
+
+
+@pytest.mark.parametrize("L,nq,nkv,off,W", [(5, 23, 23, 0, -1), (5, 23, 23, 0, 1), (4, 9, 30, 4, 2),
+                                            (7, 20, 40, 1, 0), (3, 10, 17, 2, -1)])
+def test_zero_keys_closed_form(L, nq, nkv, off, W):
+    """K = 0: every visible key weighs the same, so LSE_i = ln n_vis(i) and O_i is
+    the mean of the visible V rows.  With v_j = chunk(j), that mean is
+    sum_c n_c c / sum_c n_c over the visible chunks."""
+    rng = np.random.default_rng(1)
+    q = rng.standard_normal((1, nq, 2, 4))
+    k = np.zeros((1, nkv, 2, 4))
+    v = np.broadcast_to((np.arange(nkv) // L).astype(np.float64)[None, :, None, None],
+                        (1, nkv, 2, 4)).copy()
+    o, lse = oracle.attention(q, k, v, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=0.7)
+    for i in range(nq):
+        lo, hi = _n_visible_closed(i, L, nkv, off, W)
+        n_vis = hi - lo
+        num = 0
+        for c in range(lo // L, (hi - 1) // L + 1):
+            n_c = min(hi, (c + 1) * L) - max(lo, c * L)
+            num += n_c * c
+        assert abs(lse[0, 0, i] - math.log(n_vis)) < 1e-12
+        assert abs(o[0, i, 1, 2] - num / n_vis) < 1e-12
+
+
+def test_scale_zero_is_uniform():
+    L, n = 4, 18
+    q, k, v = _rand(1, n, n, 1, 8, seed=11)
+    o, lse = oracle.attention(q, k, v, chunk_len=L, window_chunks=1, scale=0.0)
+    for i in range(n):
+        lo, hi = _n_visible_closed(i, L, n, 0, 1)
+        assert abs(lse[0, 0, i] - math.log(hi - lo)) < 1e-12
+        np.testing.assert_allclose(o[0, i, 0], v[0, lo:hi, 0].mean(axis=0), atol=1e-12, rtol=0)
+
+
+def test_constant_values():
+    q, k, _ = _rand(1, 21, 21, 2, 8, seed=12)
+    v = np.ones((1, 21, 2, 8))
+    o, _ = oracle.attention(q, k, v, chunk_len=4, window_chunks=2, scale=0.9)
+    np.testing.assert_allclose(o, 1.0, atol=1e-14, rtol=0)
+
+
+# ---------------------------------------------------------------------------
+# invariants of the method
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("W", [-1, 1])
+def test_rows_sum_to_one(W):
+    q, k, _ = _rand(1, 40, 40, 1, 8, seed=13)
+    p = oracle.softmax_weights(q, k, chunk_len=6, window_chunks=W, scale=0.5)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-12, rtol=0)
+    vis = oracle.visibility_mask(40, 40, 6, 0, W)
+    assert np.all(p[~vis] == 0.0)
+    assert np.all(p[vis] > 0.0)
+
+
+@pytest.mark.parametrize("W", [-1, 0, 2])
+def test_causality_appending_chunks(W):
+    """Appending later chunks (more Q rows and K/V) leaves earlier rows unchanged."""
+    L = 5
+    q, k, v = _rand(1, 6 * L, 6 * L, 2, 8, seed=14)
+    full = oracle.attention(q, k, v, chunk_len=L, window_chunks=W, scale=0.4)
+    for c in range(1, 6):
+        n = c * L
+        part = oracle.attention(q[:, :n], k[:, :n], v[:, :n], chunk_len=L, window_chunks=W, scale=0.4)
+        np.testing.assert_allclose(part[0], full[0][:, :n], atol=1e-13, rtol=0)
+        np.testing.assert_allclose(part[1], full[1][:, :, :n], atol=1e-13, rtol=0)
+
+
+@pytest.mark.parametrize("W", [-1, 1, 2])
+def test_streaming_equals_parallel(W):
+    """One query chunk with q_chunk_offset = its index against the cached K/V
+    equals that chunk's rows of the parallel masked call."""
+    L, C = 6, 5
+    n = L * C - 3  # ragged last chunk
+    q, k, v = _rand(2, n, n, 2, 8, seed=15)
+    full_o, full_l = oracle.attention(q, k, v, chunk_len=L, window_chunks=W, scale=0.35)
+    for c in range(C):
+        s = slice(c * L, min((c + 1) * L, n))
+        hi = min((c + 1) * L, n)
+        so, sl = oracle.attention(q[:, s], k[:, :hi], v[:, :hi], chunk_len=L, q_chunk_offset=c,
+                                  window_chunks=W, scale=0.35)
+        np.testing.assert_allclose(so, full_o[:, s], atol=1e-13, rtol=0)
+        np.testing.assert_allclose(sl, full_l[:, :, s], atol=1e-13, rtol=0)
+
+
+def test_compacted_cache_keeps_chunk_differences():
+    """The mask depends only on chunk differences: dropping the oldest chunks a
+    window no longer sees and lowering q_chunk_offset gives the same rows."""
+    L, W = 4, 1
+    q, k, v = _rand(1, 6 * L, 6 * L, 1, 8, seed=16)
+    full_o, full_l = oracle.attention(q, k, v, chunk_len=L, window_chunks=W, scale=0.5)
+    c = 5
+    kept = slice((c - W) * L, (c + 1) * L)
+    so, sl = oracle.attention(q[:, c * L:(c + 1) * L], k[:, kept], v[:, kept], chunk_len=L,
+                              q_chunk_offset=W, window_chunks=W, scale=0.5)
+    np.testing.assert_allclose(so, full_o[:, c * L:(c + 1) * L], atol=1e-13, rtol=0)
+    np.testing.assert_allclose(sl, full_l[:, :, c * L:(c + 1) * L], atol=1e-13, rtol=0)
+
+
+def test_bidirectional_within_chunk():
+    """Permuting keys (with their values) inside one chunk leaves O unchanged:
+    no token-level triangle inside a chunk."""
+    L = 8
+    q, k, v = _rand(1, 4 * L, 4 * L, 2, 8, seed=17)
+    o, lse = oracle.attention(q, k, v, chunk_len=L, window_chunks=-1, scale=0.5)
+    perm = np.arange(4 * L)
+    rng = np.random.default_rng(3)
+    for c in range(4):
+        perm[c * L:(c + 1) * L] = c * L + rng.permutation(L)
+    o2, lse2 = oracle.attention(q, k[:, perm], v[:, perm], chunk_len=L, window_chunks=-1, scale=0.5)
+    np.testing.assert_allclose(o2, o, atol=1e-13, rtol=0)
+    np.testing.assert_allclose(lse2, lse, atol=1e-13, rtol=0)
+    # while moving a key across a chunk boundary does change the result
+    sw = np.arange(4 * L)
+    sw[L - 1], sw[L] = L, L - 1
+    o3, _ = oracle.attention(q, k[:, sw], v[:, sw], chunk_len=L, window_chunks=-1, scale=0.5)
+    assert np.abs(o3 - o).max() > 1e-3
+
+
+def test_key_shift_moves_lse_only():
+    """Adding mu to every key of a head shifts every score of query i by
+    scale * q_i . mu: O is unchanged and LSE_i moves by exactly that amount."""
+    L = 5
+    q, k, v = _rand(1, 20, 20, 2, 8, seed=18)
+    mu = np.random.default_rng(4).standard_normal((2, 8))
+    scale = 0.3
+    o, lse = oracle.attention(q, k, v, chunk_len=L, window_chunks=1, scale=scale)
+    o2, lse2 = oracle.attention(q, k + mu[None, None], v, chunk_len=L, window_chunks=1, scale=scale)
+    np.testing.assert_allclose(o2, o, atol=1e-12, rtol=0)
+    shift = scale * np.einsum("bnhd,hd->bhn", q, mu)
+    np.testing.assert_allclose(lse2 - lse, shift, atol=1e-12, rtol=0)
+
+
+def test_row_subset_matches_full():
+    q, k, v = _rand(1, 30, 30, 2, 8, seed=19)
+    o, lse = oracle.attention(q, k, v, chunk_len=7, window_chunks=2, scale=0.5)
+    rows = np.array([0, 6, 7, 13, 29])
+    o2, lse2 = oracle.attention(q, k, v, chunk_len=7, window_chunks=2, scale=0.5, rows=rows)
+    np.testing.assert_array_equal(o2, o[:, rows])
+    np.testing.assert_array_equal(lse2, lse[:, :, rows])
+
+
+def test_kv_append_oracle():
+    kc = np.zeros((2, 10, 1, 4))
+    vc = np.zeros((2, 10, 1, 4))
+    kn = np.ones((2, 3, 1, 4))
+    vn = 2 * np.ones((2, 3, 1, 4))
+    k2, v2 = oracle.kv_cache_append(kc, vc, kn, vn, cache_len=4)
+    assert k2[:, 4:7].min() == 1 and k2[:, :4].max() == 0 and k2[:, 7:].max() == 0
+    assert v2[:, 4:7].min() == 2
+    with pytest.raises(ValueError):
+        oracle.kv_cache_append(kc, vc, kn, vn, cache_len=8)
+
+
+# ---------------------------------------------------------------------------
+# the pins catch plausible mistakes planted in the oracle
+# ---------------------------------------------------------------------------
+
+def _mutant_mask(kind):
+    orig = oc.visibility_mask
+
+    def mask(nq, nkv, chunk_len, q_chunk_offset=0, window_chunks=-1, rows=None):
+        if kind == "window_off_by_one":
+            return orig(nq, nkv, chunk_len, q_chunk_offset,
+                        window_chunks + 1 if window_chunks >= 0 else -1, rows)
+        if kind == "ignore_offset":
+            return orig(nq, nkv, chunk_len, 0, window_chunks, rows)
+        if kind == "token_causal":
+            m = orig(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows)
+            r = np.arange(nq) if rows is None else np.asarray(rows)
+            return m & (np.arange(nkv)[None, :] <= (q_chunk_offset * chunk_len + r)[:, None])
+        raise ValueError(kind)
+    return mask
+
+
+@pytest.mark.parametrize("kind", ["window_off_by_one", "ignore_offset", "token_causal"])
+def test_pins_catch_planted_mask_mistakes(kind, monkeypatch):
+    monkeypatch.setattr(oc, "visibility_mask", _mutant_mask(kind))
+    with pytest.raises(AssertionError):
+        check_hand_example(oc.attention)
+
+
+def test_pins_catch_transposed_scores(monkeypatch):
+    """A transposed score matrix (K Q^T instead of Q K^T) fails the brute-force pin."""
+    def bad(q, k, v, chunk_len, q_chunk_offset=0, window_chunks=-1, scale=None, rows=None, block=512):
+        return oc.attention(k, q, v, chunk_len, q_chunk_offset, window_chunks, scale, rows, block)
+    q, k, v = _rand(1, 12, 12, 1, 4, seed=20)
+    o1, _ = bad(q, k, v, chunk_len=4, window_chunks=1, scale=0.5)
+    o2, _ = oracle.brute_force(q, k, v, 1, 4, 0, 1, scale=0.5)
+    assert np.abs(o1 - o2).max() > 1e-6
