@@ -1,0 +1,127 @@
+/*
+ * fastvr.h -- C ABI of the chunk-wise causal attention library (libfastvr.so).
+ *
+ * The operation is the chunk-wise causal self-attention of FastVR
+ * (arXiv 2609.36757, Sec. 3.1, Eq. 1 and the paragraph that follows it):
+ * latent tokens, flattened frame-major, are grouped into temporal chunks of
+ * `chunk_len` tokens; a query in chunk c sees every key of chunks
+ * c - window_chunks .. c (bidirectional inside a chunk, nothing from later
+ * chunks).  Eq. 1 is window_chunks = 1; window_chunks = -1 lifts the lower
+ * bound (an unbounded causal prefix of chunks).  The same call serves the
+ * parallel form over a whole sequence and the streaming form, where one new
+ * query chunk attends to a KV cache (q_chunk_offset = that chunk's index
+ * relative to the first cached chunk; only chunk differences matter).
+ *
+ *   LSE_i = ln sum_{j visible to i} exp(scale * q_i . k_j)
+ *   O_i   = sum_{j visible to i} exp(scale * q_i . k_j - LSE_i) * v_j
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *    allocates nothing, keeps no pointer after returning, has no global mutable
+ *    state besides a thread-local error string, and is re-entrant.
+ *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.  Calls
+ *    return after enqueueing; work is ordered on `stream`.  Faults during
+ *    execution surface at the caller's next synchronisation of that stream.
+ *  - Every argument is validated on the host BEFORE any HIP call.  A failing
+ *    check returns a non-zero status, enqueues nothing, and leaves a message
+ *    for fastvr_last_error().  No entry point throws or aborts.
+ *  - Element types: bf16 inputs (16-bit brain float, round-to-nearest-even
+ *    produced by the caller), fp32 outputs.
+ */
+#ifndef FASTVR_H
+#define FASTVR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FASTVR_ABI_VERSION 1
+
+typedef enum {
+  FASTVR_OK = 0,
+  FASTVR_ERR_INVALID_ARGUMENT = 1, /* null/misaligned pointer, bad size, offset, window, stride or scale */
+  FASTVR_ERR_UNSUPPORTED = 2,      /* head_dim not in {64, 128}, or a problem too large for one launch */
+  FASTVR_ERR_CAPACITY = 3,         /* a KV append would overflow the cache */
+  FASTVR_ERR_HIP = 4               /* the HIP runtime refused a launch */
+} fastvr_status;
+
+/*
+ * Chunk-causal attention forward (Sec. 3.1, Eq. 1; streaming form: last
+ * paragraph of Sec. 3.1).
+ *
+ *   q   bf16 [B, Nq,  H, d] contiguous     query rows
+ *   k   bf16 [B, Nkv, H, d] contiguous     key rows
+ *   v   bf16 [B, Nkv, H, d] contiguous     value rows
+ *   o   fp32 [B, Nq,  H, d] contiguous     output, fully overwritten
+ *   lse fp32 [B, H, Nq]     contiguous     natural-log sum-exp per row, or NULL
+ *
+ * Query row i lies in chunk q_chunk_offset + i / chunk_len; key row j in chunk
+ * j / chunk_len.  Keys of later chunks may be present in k/v; they are masked.
+ *
+ * Preconditions (else FASTVR_ERR_INVALID_ARGUMENT unless noted):
+ *  - q, k, v, o non-NULL and 16-byte aligned; lse NULL or 4-byte aligned;
+ *    o does not overlap q, k or v;
+ *  - B, H, Nq, Nkv, chunk_len >= 0 and q_chunk_offset >= 0, with
+ *    q_chunk_offset * chunk_len + Nq <= Nkv (every query sees its own key, so
+ *    no softmax row is empty) and chunk_len >= 1 when Nq > 0;
+ *  - d in {64, 128} (else FASTVR_ERR_UNSUPPORTED);
+ *  - window_chunks >= -1;  scale finite;
+ *  - no element count overflows int64.
+ * B, H or Nq equal to 0 is an empty problem: FASTVR_OK, nothing enqueued.
+ */
+fastvr_status fastvr_chunk_attn_fwd(const void* q, const void* k, const void* v, float* o,
+                                    float* lse, int64_t B, int64_t H, int64_t Nq, int64_t Nkv,
+                                    int64_t d, int64_t chunk_len, int64_t q_chunk_offset,
+                                    int64_t window_chunks, float scale, void* stream);
+
+/*
+ * Same operation with explicit element strides, for tensors that are views
+ * (e.g. a KV cache [B, capacity, H, d] with capacity > Nkv and B > 1).
+ * Within a token, heads are contiguous with stride d and head_dim elements are
+ * contiguous.  Strides are in elements: *_sb between batches, *_st between
+ * tokens.  The bf16 strides must be multiples of 8 and the fp32 ones of 4
+ * (16-byte rows), and each must be >= H * d.  lse is [B, H, Nq] contiguous.
+ */
+fastvr_status fastvr_chunk_attn_fwd_ex(const void* q, int64_t q_sb, int64_t q_st,
+                                       const void* k, int64_t k_sb, int64_t k_st,
+                                       const void* v, int64_t v_sb, int64_t v_st,
+                                       float* o, int64_t o_sb, int64_t o_st, float* lse,
+                                       int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                                       int64_t chunk_len, int64_t q_chunk_offset,
+                                       int64_t window_chunks, float scale, void* stream);
+
+/*
+ * KV-cache append for streaming inference with KV caching (Sec. 3.1, last
+ * paragraph): copies the new chunk's keys and values
+ *   k_new, v_new  bf16 [B, n_new, H, d] contiguous
+ * into the caches
+ *   k_cache, v_cache  bf16 [B, capacity, H, d] contiguous
+ * at token offset cache_len (tokens cache_len .. cache_len + n_new - 1 of each
+ * batch).  Nothing is evicted; the caller tracks cache_len.
+ * Preconditions: pointers non-NULL and 16-byte aligned, caches not overlapping
+ * the new tensors; B, H, capacity, cache_len, n_new >= 0; d in {64, 128};
+ * cache_len + n_new <= capacity (else FASTVR_ERR_CAPACITY).
+ * n_new, B or H equal to 0: FASTVR_OK, nothing enqueued.
+ */
+fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k_new,
+                                     const void* v_new, int64_t B, int64_t H, int64_t d,
+                                     int64_t capacity, int64_t cache_len, int64_t n_new,
+                                     void* stream);
+
+/* Static string naming a status code ("FASTVR_OK", ...); never NULL. */
+const char* fastvr_status_string(fastvr_status s);
+
+/* Detail of the last failing call on this thread ("" if none).  The pointer is
+   valid until the next library call on the same thread. */
+const char* fastvr_last_error(void);
+
+/* FASTVR_ABI_VERSION of the built library. */
+int fastvr_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTVR_H */

@@ -97,6 +97,17 @@ def _as_f64(x) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 
 
+def _head_f64(x, b: int, h: int, rows=None) -> np.ndarray:
+    """x[b, rows, h, :] widened to float64 (rows=None: all rows)."""
+    if hasattr(x, "detach"):
+        import torch
+        sl = x[b, :, h, :] if rows is None else x[b, torch.as_tensor(rows), h, :]
+        return sl.detach().to("cpu", torch.float64).numpy()
+    x = np.asarray(x)
+    sl = x[b, :, h, :] if rows is None else x[b, rows, h, :]
+    return np.asarray(sl, dtype=np.float64)
+
+
 def attention(q, k, v, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
               scale: float | None = None, rows=None, block: int = 512):
     """Chunk-causal attention in fp64.
@@ -108,9 +119,6 @@ def attention(q, k, v, chunk_len: int, q_chunk_offset: int = 0, window_chunks: i
     Per (b, h) and block of query rows: S = scale * Q K^T, S = -inf where the mask
     hides the key, m = rowmax S, P = exp(S - m), l = rowsum P, O = P V / l,
     LSE = m + ln l."""
-    q = _as_f64(q)
-    k = _as_f64(k)
-    v = _as_f64(v)
     B, nq, H, d = q.shape
     nkv = k.shape[1]
     if scale is None:
@@ -120,19 +128,21 @@ def attention(q, k, v, chunk_len: int, q_chunk_offset: int = 0, window_chunks: i
     R = rows.shape[0]
     o = np.zeros((B, R, H, d), dtype=np.float64)
     lse = np.zeros((B, H, R), dtype=np.float64)
-    for r0 in range(0, R, block):
-        rr = rows[r0:r0 + block]
-        vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows=rr)
-        if not vis.any(axis=1).all():
-            raise ValueError("a query row has no visible key")
-        for b in range(B):
-            for h in range(H):
-                s = scale * (q[b, rr, h, :] @ k[b, :, h, :].T)
+    for b in range(B):
+        for h in range(H):
+            kh = _head_f64(k, b, h)
+            vh = _head_f64(v, b, h)
+            for r0 in range(0, R, block):
+                rr = rows[r0:r0 + block]
+                vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows=rr)
+                if not vis.any(axis=1).all():
+                    raise ValueError("a query row has no visible key")
+                s = scale * (_head_f64(q, b, h, rr) @ kh.T)
                 s = np.where(vis, s, -np.inf)
                 m = s.max(axis=1, keepdims=True)
                 p = np.exp(s - m)
                 l = p.sum(axis=1, keepdims=True)
-                o[b, r0:r0 + len(rr), h, :] = (p @ v[b, :, h, :]) / l
+                o[b, r0:r0 + len(rr), h, :] = (p @ vh) / l
                 lse[b, h, r0:r0 + len(rr)] = (m + np.log(l))[:, 0]
     return o, lse
 

@@ -1,0 +1,231 @@
+// C ABI of libfastvr.so: argument validation (entirely on the host, before any
+// HIP call), status strings, the thread-local error detail, and dispatch to
+// the kernel launchers.  Declarations and the contract: include/fastvr.h.
+#include "fastvr.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fastvr_status fail(fastvr_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+fastvr_status ok() {
+  g_last_error.clear();
+  return FASTVR_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// a * b with an overflow check on non-negative int64
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+bool add_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0 || a > INT64_MAX - b) return false;
+  *out = a + b;
+  return true;
+}
+
+// Byte extent of a [B, N, H*d] view with element strides (sb, st): the last
+// element touched is (B-1)*sb + (N-1)*st + H*d - 1.
+bool extent_bytes(int64_t B, int64_t N, int64_t sb, int64_t st, int64_t hd, int64_t elem, int64_t* out) {
+  int64_t a, b, c;
+  if (!mul_ok(B - 1, sb, &a) || !mul_ok(N - 1, st, &b) || !add_ok(a, b, &c) || !add_ok(c, hd, &c)) return false;
+  return mul_ok(c, elem, out);
+}
+
+bool overlap(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + static_cast<uintptr_t>(nb) && y < x + static_cast<uintptr_t>(na);
+}
+
+struct View {
+  const char* name;
+  const void* ptr;
+  int64_t sb, st, n;
+  int64_t elem;  // bytes per element
+};
+
+fastvr_status check_view(const View& w, int64_t B, int64_t hd, int64_t* bytes) {
+  if (w.ptr == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is NULL", w.name);
+  if (!aligned(w.ptr, 16)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", w.name);
+  const int64_t unit = 16 / w.elem;
+  if (w.st < hd) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s token stride %lld < H*d = %lld", w.name,
+                             (long long)w.st, (long long)hd);
+  if (w.st % unit != 0 || w.sb % unit != 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s strides must be multiples of %lld elements", w.name, (long long)unit);
+  if (B > 1) {
+    int64_t span;
+    if (!mul_ok(w.n, w.st, &span)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s size overflows int64", w.name);
+    if (w.sb < span)
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s batch stride %lld < N * token stride = %lld", w.name,
+                  (long long)w.sb, (long long)span);
+  }
+  if (!extent_bytes(B, w.n, w.sb, w.st, hd, w.elem, bytes))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s size overflows int64", w.name);
+  return FASTVR_OK;
+}
+
+fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k, int64_t k_sb, int64_t k_st,
+                       const void* v, int64_t v_sb, int64_t v_st, float* o, int64_t o_sb, int64_t o_st, float* lse,
+                       int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
+                       int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+  if (B < 0 || H < 0 || Nq < 0 || Nkv < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld H=%lld Nq=%lld Nkv=%lld)", (long long)B,
+                (long long)H, (long long)Nq, (long long)Nkv);
+  if (d != 64 && d != 128) return fail(FASTVR_ERR_UNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)d);
+  if (q_chunk_offset < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "q_chunk_offset %lld < 0", (long long)q_chunk_offset);
+  if (window_chunks < -1)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "window_chunks %lld < -1", (long long)window_chunks);
+  if (!std::isfinite(scale)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "scale is not finite");
+  if (B == 0 || H == 0 || Nq == 0) return ok();  // empty problem
+  if (chunk_len < 1) return fail(FASTVR_ERR_INVALID_ARGUMENT, "chunk_len %lld < 1", (long long)chunk_len);
+  int64_t first_q, last_q;
+  if (!mul_ok(q_chunk_offset, chunk_len, &first_q) || !add_ok(first_q, Nq, &last_q))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "q_chunk_offset * chunk_len + Nq overflows int64");
+  if (last_q > Nkv)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT,
+                "q_chunk_offset * chunk_len + Nq = %lld > Nkv = %lld (a query would not see its own key)",
+                (long long)last_q, (long long)Nkv);
+  if (Nkv > INT32_MAX || Nq > INT32_MAX || B > INT32_MAX || H > INT32_MAX)
+    return fail(FASTVR_ERR_UNSUPPORTED, "sizes must be below 2^31");
+  int64_t hd, bh;
+  if (!mul_ok(H, d, &hd) || !mul_ok(B, H, &bh)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+
+  int64_t qb, kb, vb, ob;
+  fastvr_status s;
+  if ((s = check_view({"q", q, q_sb, q_st, Nq, 2}, B, hd, &qb)) != FASTVR_OK) return s;
+  if ((s = check_view({"k", k, k_sb, k_st, Nkv, 2}, B, hd, &kb)) != FASTVR_OK) return s;
+  if ((s = check_view({"v", v, v_sb, v_st, Nkv, 2}, B, hd, &vb)) != FASTVR_OK) return s;
+  if ((s = check_view({"o", o, o_sb, o_st, Nq, 4}, B, hd, &ob)) != FASTVR_OK) return s;
+  int64_t lb = 0;
+  if (lse != nullptr) {
+    if (!aligned(lse, 4)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse is not 4-byte aligned");
+    if (!mul_ok(bh, Nq, &lb) || !mul_ok(lb, 4, &lb)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse size overflows");
+  }
+  if (overlap(o, ob, q, qb) || overlap(o, ob, k, kb) || overlap(o, ob, v, vb))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "o overlaps q, k or v");
+  if (lse != nullptr && (overlap(lse, lb, q, qb) || overlap(lse, lb, k, kb) || overlap(lse, lb, v, vb) ||
+                         overlap(lse, lb, o, ob)))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse overlaps q, k, v or o");
+
+  const fastvr::FwdGrid g = fastvr::fwd_grid(B, H, Nq, chunk_len);
+  if (g.n_items > fastvr::kMaxFwdItems)
+    return fail(FASTVR_ERR_UNSUPPORTED, "problem needs %lld workgroups (> %lld)", (long long)g.n_items,
+                (long long)fastvr::kMaxFwdItems);
+
+  fastvr::FwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
+  a.q_sb = q_sb; a.q_st = q_st;
+  a.k_sb = k_sb; a.k_st = k_st;
+  a.v_sb = v_sb; a.v_st = v_st;
+  a.o_sb = o_sb; a.o_st = o_st;
+  a.B = B; a.H = H; a.nq = Nq; a.nkv = Nkv; a.d = d;
+  a.chunk_len = chunk_len;
+  a.q_chunk_offset = q_chunk_offset;
+  a.window_chunks = window_chunks;
+  a.scale = scale;
+  const hipError_t e = fastvr::launch_chunk_attn_fwd(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "chunk_attn_fwd launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+fastvr_status fastvr_chunk_attn_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int64_t B,
+                                    int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
+                                    int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+  int64_t hd = 0, sq = 0, skv = 0;
+  if (H >= 0 && d >= 0 && Nq >= 0 && Nkv >= 0 &&
+      (!mul_ok(H, d, &hd) || !mul_ok(Nq, hd, &sq) || !mul_ok(Nkv, hd, &skv)))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  return fwd_impl(q, sq, hd, k, skv, hd, v, skv, hd, o, sq, hd, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+                  window_chunks, scale, stream);
+}
+
+fastvr_status fastvr_chunk_attn_fwd_ex(const void* q, int64_t q_sb, int64_t q_st, const void* k, int64_t k_sb,
+                                       int64_t k_st, const void* v, int64_t v_sb, int64_t v_st, float* o,
+                                       int64_t o_sb, int64_t o_st, float* lse, int64_t B, int64_t H, int64_t Nq,
+                                       int64_t Nkv, int64_t d, int64_t chunk_len, int64_t q_chunk_offset,
+                                       int64_t window_chunks, float scale, void* stream) {
+  return fwd_impl(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, B, H, Nq, Nkv, d, chunk_len,
+                  q_chunk_offset, window_chunks, scale, stream);
+}
+
+fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new, int64_t B,
+                                     int64_t H, int64_t d, int64_t capacity, int64_t cache_len, int64_t n_new,
+                                     void* stream) {
+  if (B < 0 || H < 0 || capacity < 0 || cache_len < 0 || n_new < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size");
+  if (d != 64 && d != 128) return fail(FASTVR_ERR_UNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)d);
+  int64_t end;
+  if (!add_ok(cache_len, n_new, &end)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "cache_len + n_new overflows");
+  if (end > capacity)
+    return fail(FASTVR_ERR_CAPACITY, "cache_len + n_new = %lld > capacity = %lld", (long long)end,
+                (long long)capacity);
+  if (B == 0 || H == 0 || n_new == 0) return ok();
+  if (B > 65535) return fail(FASTVR_ERR_UNSUPPORTED, "B = %lld > 65535", (long long)B);
+  const void* ptrs[4] = {k_cache, v_cache, k_new, v_new};
+  const char* names[4] = {"k_cache", "v_cache", "k_new", "v_new"};
+  for (int i = 0; i < 4; ++i) {
+    if (ptrs[i] == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is NULL", names[i]);
+    if (!aligned(ptrs[i], 16)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", names[i]);
+  }
+  int64_t hd, cache_bytes, new_bytes;
+  if (!mul_ok(H, d, &hd) || !mul_ok(B, capacity, &cache_bytes) || !mul_ok(cache_bytes, hd, &cache_bytes) ||
+      !mul_ok(cache_bytes, 2, &cache_bytes) || !mul_ok(B, n_new, &new_bytes) || !mul_ok(new_bytes, hd, &new_bytes) ||
+      !mul_ok(new_bytes, 2, &new_bytes))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  if (overlap(k_cache, cache_bytes, v_cache, cache_bytes))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "k_cache and v_cache overlap");
+  for (int c = 0; c < 2; ++c)
+    for (int n = 2; n < 4; ++n)
+      if (overlap(ptrs[c], cache_bytes, ptrs[n], new_bytes))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s overlaps %s", names[c], names[n]);
+  const hipError_t e = fastvr::launch_kv_append(k_cache, v_cache, k_new, v_new, B, H, d, capacity, cache_len, n_new,
+                                                static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "kv_append launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+const char* fastvr_status_string(fastvr_status s) {
+  switch (s) {
+    case FASTVR_OK: return "FASTVR_OK";
+    case FASTVR_ERR_INVALID_ARGUMENT: return "FASTVR_ERR_INVALID_ARGUMENT";
+    case FASTVR_ERR_UNSUPPORTED: return "FASTVR_ERR_UNSUPPORTED";
+    case FASTVR_ERR_CAPACITY: return "FASTVR_ERR_CAPACITY";
+    case FASTVR_ERR_HIP: return "FASTVR_ERR_HIP";
+  }
+  return "FASTVR_ERR_UNKNOWN";
+}
+
+const char* fastvr_last_error(void) { return g_last_error.c_str(); }
+
+int fastvr_abi_version(void) { return FASTVR_ABI_VERSION; }
+
+}  // extern "C"

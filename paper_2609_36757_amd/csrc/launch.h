@@ -1,0 +1,44 @@
+// Internal launch interface between the C-ABI layer and the HIP kernels.
+// Arguments reaching these functions have already been validated.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace fastvr {
+
+struct FwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  float* o;
+  float* lse;            // may be null
+  int64_t q_sb, q_st;    // element strides: batch, token (bf16)
+  int64_t k_sb, k_st;
+  int64_t v_sb, v_st;
+  int64_t o_sb, o_st;    // fp32
+  int64_t B, H, nq, nkv, d;
+  int64_t chunk_len, q_chunk_offset, window_chunks;
+  float scale;
+};
+
+// Work decomposition of one forward call (host side, also used for checks).
+struct FwdGrid {
+  int64_t n_local_chunks;  // query chunks touched by the call
+  int64_t tiles_full;      // query tiles of a full chunk
+  int64_t tiles_last;      // query tiles of the last (possibly ragged) chunk
+  int64_t n_items;         // workgroups
+};
+
+constexpr int kFwdThreads = 512;  // 8 wave64 per workgroup
+constexpr int kFwdRowsPerItem = 256;
+constexpr int64_t kMaxFwdItems = (int64_t(1) << 32) / kFwdThreads - 1;
+
+FwdGrid fwd_grid(int64_t B, int64_t H, int64_t nq, int64_t chunk_len);
+hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream);
+
+hipError_t launch_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
+                            int64_t B, int64_t H, int64_t d, int64_t capacity, int64_t cache_len,
+                            int64_t n_new, hipStream_t stream);
+
+}  // namespace fastvr

@@ -1,0 +1,168 @@
+"""ctypes binding of libfastvr.so (declared in include/fastvr.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of the library.  torch tensors provide device memory and the stream.
+If the library is missing, every call raises; there is no fallback."""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libfastvr.so")
+
+OK = 0
+ERR_INVALID_ARGUMENT = 1
+ERR_UNSUPPORTED = 2
+ERR_CAPACITY = 3
+ERR_HIP = 4
+
+EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
+            "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
+
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+_LIB = None
+
+
+class FastVRError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def load() -> ctypes.CDLL:
+    """Load the in-tree libfastvr.so (built by ``python -m paper_2609_36757_amd.build``)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_36757_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.fastvr_chunk_attn_fwd.restype = ctypes.c_int
+    lib.fastvr_chunk_attn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
+                                          _i64, ctypes.c_float, _vp]
+    lib.fastvr_chunk_attn_fwd_ex.restype = ctypes.c_int
+    lib.fastvr_chunk_attn_fwd_ex.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64,
+                                             _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
+                                             ctypes.c_float, _vp]
+    lib.fastvr_kv_cache_append.restype = ctypes.c_int
+    lib.fastvr_kv_cache_append.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _vp]
+    lib.fastvr_status_string.restype = ctypes.c_char_p
+    lib.fastvr_status_string.argtypes = [ctypes.c_int]
+    lib.fastvr_last_error.restype = ctypes.c_char_p
+    lib.fastvr_last_error.argtypes = []
+    lib.fastvr_abi_version.restype = ctypes.c_int
+    lib.fastvr_abi_version.argtypes = []
+    _LIB = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        lib = load()
+        name = lib.fastvr_status_string(status).decode()
+        detail = lib.fastvr_last_error().decode()
+        raise FastVRError(status, f"{name}: {detail}")
+
+
+def last_error() -> str:
+    return load().fastvr_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+# raw entry points (integers for pointers; used by the tests and the bench)
+# ---------------------------------------------------------------------------
+
+def fwd_raw(q, k, v, o, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks, scale,
+            stream=0) -> int:
+    return load().fastvr_chunk_attn_fwd(q, k, v, o, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+                                        window_chunks, scale, stream)
+
+
+def fwd_ex_raw(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, B, H, Nq, Nkv, d,
+               chunk_len, q_chunk_offset, window_chunks, scale, stream=0) -> int:
+    return load().fastvr_chunk_attn_fwd_ex(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse,
+                                           B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks,
+                                           scale, stream)
+
+
+def append_raw(k_cache, v_cache, k_new, v_new, B, H, d, capacity, cache_len, n_new, stream=0) -> int:
+    return load().fastvr_kv_cache_append(k_cache, v_cache, k_new, v_new, B, H, d, capacity, cache_len,
+                                         n_new, stream)
+
+
+# ---------------------------------------------------------------------------
+# torch-facing wrappers
+# ---------------------------------------------------------------------------
+
+def _stream_handle(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _bnhd_strides(t, name):
+    """(batch stride, token stride) of a [B, N, H, d] view whose heads and dims
+    are packed (stride(3) == 1, stride(2) == d)."""
+    if t.dim() != 4:
+        raise ValueError(f"{name} must be 4-D [B, N, H, d]")
+    if t.stride(3) != 1 or t.stride(2) != t.shape[3]:
+        raise ValueError(f"{name}: heads and head_dim must be contiguous (stride(2) == d, stride(3) == 1)")
+    return t.stride(0), t.stride(1)
+
+
+def chunk_attn(q, k, v, *, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
+               scale: float | None = None, out=None, lse=None, return_lse: bool = True, stream=None):
+    """Chunk-causal attention forward (FastVR Sec. 3.1, Eq. 1).
+
+    q [B, Nq, H, d], k/v [B, Nkv, H, d] bf16 CUDA tensors (views allowed when
+    heads and head_dim are packed).  Returns (o fp32 [B, Nq, H, d], lse fp32
+    [B, H, Nq] or None)."""
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda:
+            raise ValueError(f"{name} must be a bfloat16 GPU tensor")
+    B, Nq, H, d = q.shape
+    Nkv = k.shape[1]
+    if k.shape != (B, Nkv, H, d) or v.shape != k.shape:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty((B, Nq, H, d), dtype=torch.float32, device=q.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != (B, Nq, H, d):
+        raise ValueError("out must be float32 [B, Nq, H, d]")
+    if return_lse and lse is None:
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, Nq)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [B, H, Nq] tensor")
+    lse_ptr = lse.data_ptr() if lse is not None else None
+    st = _stream_handle(stream)
+    if all(t.is_contiguous() for t in (q, k, v, out)):
+        status = fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse_ptr, B, H, Nq, Nkv, d,
+                         chunk_len, q_chunk_offset, window_chunks, scale, st)
+    else:
+        qs, ks, vs, os_ = (_bnhd_strides(t, n) for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out")))
+        status = fwd_ex_raw(q.data_ptr(), *qs, k.data_ptr(), *ks, v.data_ptr(), *vs, out.data_ptr(), *os_,
+                            lse_ptr, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks, scale, st)
+    _check(status)
+    return out, lse
+
+
+def kv_cache_append(k_cache, v_cache, k_new, v_new, cache_len: int, stream=None) -> int:
+    """Copy k_new/v_new [B, n_new, H, d] into the contiguous caches [B, capacity, H, d]
+    at token offset cache_len; returns the new cache length."""
+    import torch
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("k_new", k_new), ("v_new", v_new)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor")
+    B, cap, H, d = k_cache.shape
+    n_new = k_new.shape[1]
+    if v_cache.shape != k_cache.shape or k_new.shape != (B, n_new, H, d) or v_new.shape != k_new.shape:
+        raise ValueError("cache / new-chunk shape mismatch")
+    _check(append_raw(k_cache.data_ptr(), v_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), B, H, d, cap,
+                      cache_len, n_new, _stream_handle(stream)))
+    return cache_len + n_new

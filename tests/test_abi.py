@@ -1,0 +1,194 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any HIP call
+(so no call here reaches the runtime; fake device addresses are never used)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36757_amd import fastvr
+from paper_2609_36757_amd import workloads
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fastvr.h")
+
+# Distinct fake addresses, 1 TiB apart, for calls that must fail validation:
+# every case below is rejected on the host before the HIP runtime is touched.
+Q, K, V, O, LSE = ((i + 1) << 40 for i in range(5))
+BIG = 1 << 62
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fastvr_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fastvr.LIB_PATH):
+        pytest.fail("libfastvr.so is not built (run `python -m paper_2609_36757_amd.build`)")
+    return fastvr.load()
+
+
+def test_header_symbols_exported(lib):
+    declared = _declared_functions()
+    assert set(declared) == set(fastvr.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_version_and_status_strings(lib):
+    assert lib.fastvr_abi_version() == 1
+    assert lib.fastvr_status_string(0) == b"FASTVR_OK"
+    assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
+    assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
+    assert lib.fastvr_status_string(3) == b"FASTVR_ERR_CAPACITY"
+    assert lib.fastvr_status_string(4) == b"FASTVR_ERR_HIP"
+    assert lib.fastvr_status_string(99) == b"FASTVR_ERR_UNKNOWN"
+
+
+GOOD = dict(q=Q, k=K, v=V, o=O, lse=LSE, B=1, H=2, Nq=64, Nkv=64, d=64, chunk_len=16, q_chunk_offset=0,
+            window_chunks=-1, scale=0.125)
+
+
+def _fwd(**kw):
+    a = dict(GOOD)
+    a.update(kw)
+    return fastvr.fwd_raw(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["H"], a["Nq"], a["Nkv"], a["d"],
+                          a["chunk_len"], a["q_chunk_offset"], a["window_chunks"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(q=None), fastvr.ERR_INVALID_ARGUMENT, "q is NULL"),
+    (dict(k=None), fastvr.ERR_INVALID_ARGUMENT, "k is NULL"),
+    (dict(v=None), fastvr.ERR_INVALID_ARGUMENT, "v is NULL"),
+    (dict(o=None), fastvr.ERR_INVALID_ARGUMENT, "o is NULL"),
+    (dict(q=Q + 8), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (dict(o=O + 4), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (dict(lse=LSE + 2), fastvr.ERR_INVALID_ARGUMENT, "lse is not 4-byte aligned"),
+    (dict(B=-1), fastvr.ERR_INVALID_ARGUMENT, "negative size"),
+    (dict(Nkv=-5), fastvr.ERR_INVALID_ARGUMENT, "negative size"),
+    (dict(d=96), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(d=256), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(chunk_len=0), fastvr.ERR_INVALID_ARGUMENT, "chunk_len"),
+    (dict(q_chunk_offset=-1), fastvr.ERR_INVALID_ARGUMENT, "q_chunk_offset"),
+    (dict(window_chunks=-2), fastvr.ERR_INVALID_ARGUMENT, "window_chunks"),
+    (dict(scale=float("nan")), fastvr.ERR_INVALID_ARGUMENT, "scale"),
+    (dict(scale=float("inf")), fastvr.ERR_INVALID_ARGUMENT, "scale"),
+    (dict(Nkv=63), fastvr.ERR_INVALID_ARGUMENT, "would not see its own key"),
+    (dict(Nq=16, q_chunk_offset=4), fastvr.ERR_INVALID_ARGUMENT, "would not see its own key"),
+    (dict(q_chunk_offset=BIG, chunk_len=16), fastvr.ERR_INVALID_ARGUMENT, "overflows"),
+    (dict(Nq=BIG, Nkv=BIG), fastvr.ERR_INVALID_ARGUMENT, "overflows"),
+    (dict(Nq=1 << 31, Nkv=1 << 31), fastvr.ERR_UNSUPPORTED, "2^31"),
+    (dict(o=Q + 64), fastvr.ERR_INVALID_ARGUMENT, "overlaps"),
+    (dict(lse=O + 16), fastvr.ERR_INVALID_ARGUMENT, "overlaps"),
+])
+def test_fwd_rejects(lib, kw, status, needle):
+    assert _fwd(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+def test_fwd_too_many_workgroups(lib):
+    # chunk_len 1 -> one 256-row tile per query row: B*H*Nq = 2^23 items exceed one launch
+    assert _fwd(B=1, H=64, Nq=1 << 17, Nkv=1 << 17, chunk_len=1) == fastvr.ERR_UNSUPPORTED
+    assert "workgroups" in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(Nq=0), dict(B=0), dict(H=0), dict(Nq=0, q=None, o=None)])
+def test_fwd_empty_problem_is_ok(lib, kw):
+    assert _fwd(**kw) == fastvr.OK
+    assert fastvr.last_error() == ""
+
+
+def _fwd_ex(**kw):
+    a = dict(GOOD, B=2, q_sb=64 * 128, q_st=128, k_sb=64 * 128, k_st=128, v_sb=64 * 128, v_st=128,
+             o_sb=64 * 128, o_st=128)
+    a.update(kw)
+    return fastvr.fwd_ex_raw(a["q"], a["q_sb"], a["q_st"], a["k"], a["k_sb"], a["k_st"], a["v"], a["v_sb"],
+                             a["v_st"], a["o"], a["o_sb"], a["o_st"], a["lse"], a["B"], a["H"], a["Nq"], a["Nkv"],
+                             a["d"], a["chunk_len"], a["q_chunk_offset"], a["window_chunks"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(q_st=64), "token stride"),
+    (dict(k_st=132), "multiples of 8"),
+    (dict(o_st=130), "multiples of 4"),
+    (dict(v_sb=100 * 128 + 4), "multiples of 8"),
+    (dict(o_sb=63 * 128), "batch stride"),
+    (dict(k_sb=BIG, k_st=BIG // 4), "overflows"),
+])
+def test_fwd_ex_rejects_bad_strides(lib, kw, needle):
+    assert _fwd_ex(**kw) == fastvr.ERR_INVALID_ARGUMENT
+    assert needle in fastvr.last_error()
+
+
+def _app(**kw):
+    a = dict(kc=Q, vc=K, kn=V, vn=O, B=1, H=2, d=64, capacity=100, cache_len=10, n_new=20)
+    a.update(kw)
+    return fastvr.append_raw(a["kc"], a["vc"], a["kn"], a["vn"], a["B"], a["H"], a["d"], a["capacity"],
+                             a["cache_len"], a["n_new"], None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(capacity=29), fastvr.ERR_CAPACITY, "capacity"),
+    (dict(cache_len=81), fastvr.ERR_CAPACITY, "capacity"),
+    (dict(kc=None), fastvr.ERR_INVALID_ARGUMENT, "k_cache is NULL"),
+    (dict(vn=None), fastvr.ERR_INVALID_ARGUMENT, "v_new is NULL"),
+    (dict(kn=V + 2), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (dict(d=32), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(n_new=-1), fastvr.ERR_INVALID_ARGUMENT, "negative"),
+    (dict(cache_len=BIG, n_new=BIG, capacity=BIG), fastvr.ERR_INVALID_ARGUMENT, "overflows"),
+    (dict(vc=Q + 256), fastvr.ERR_INVALID_ARGUMENT, "overlap"),
+    (dict(kn=Q + 1024), fastvr.ERR_INVALID_ARGUMENT, "overlaps"),
+    (dict(B=70000, capacity=30), fastvr.ERR_UNSUPPORTED, "65535"),
+])
+def test_append_rejects(lib, kw, status, needle):
+    assert _app(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(n_new=0), dict(B=0), dict(H=0)])
+def test_append_empty_is_ok(lib, kw):
+    assert _app(**kw) == fastvr.OK
+
+
+def test_error_is_thread_local(lib):
+    import threading
+    assert _fwd(d=96) == fastvr.ERR_UNSUPPORTED
+    seen = {}
+
+    def other():
+        seen["msg"] = fastvr.last_error()
+    th = threading.Thread(target=other)
+    th.start()
+    th.join()
+    assert seen["msg"] == ""
+    assert "head_dim" in fastvr.last_error()
+
+
+def test_wrapper_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(fastvr, "_LIB", None)
+    monkeypatch.setattr(fastvr, "LIB_PATH", "/nonexistent/libfastvr.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        fastvr.load()
+
+
+def test_input_generator_is_deterministic():
+    a = workloads.make_qkv(1, 33, 40, 2, 64, seed=9)
+    b = workloads.make_qkv(1, 33, 40, 2, 64, seed=9)
+    c = workloads.make_qkv(1, 33, 40, 2, 64, seed=10)
+    for x, y in zip(a, b):
+        assert x.dtype == workloads.torch.bfloat16
+        assert workloads.torch.equal(x, y)
+    assert not workloads.torch.equal(a[0], c[0])
+
+
+def test_workload_registry_shapes():
+    w = workloads.WORKLOADS
+    assert (w["1080p"].n_tokens, w["1080p"].chunk_len, w["1080p"].n_chunks) == (65280, 16320, 4)
+    assert (w["480p"].n_tokens, w["480p"].chunk_len, w["480p"].n_chunks) == (18720, 3120, 6)
+    assert (w["wide_sw"].n_tokens, w["wide_sw"].window_chunks, w["wide_sw"].n_chunks) == (138720, 2, 9)
+    assert w["1080p_stream"].stream_chunk == 3 and w["1080p_stream"].seed == w["1080p"].seed
+    assert w["tiny"].d == 64 and w["tiny"].scale == 0.125

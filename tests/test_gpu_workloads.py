@@ -1,0 +1,100 @@
+"""Parity at the full sizes of the benchmark workloads, in the launch
+configuration the benchmark times.  The oracle evaluates a stratified sample
+of query rows (every chunk and 256-row tile boundary, the ragged tail, and
+seeded random rows); the streaming step is also checked bit for bit against
+the parallel call over the whole sequence."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_36757_amd import fastvr
+from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence, streaming_views
+
+from parity import compare, run_oracle, sample_rows, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fastvr.load()
+    return torch.device("cuda:0")
+
+
+def _announce(label):
+    print(f"\n[gpu case] {label}", flush=True)
+
+
+def _full_call(w, q, k, v, dev):
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    o, lse = fastvr.chunk_attn(qd, kd, vd, chunk_len=w.chunk_len, window_chunks=w.window_chunks, scale=w.scale)
+    torch.cuda.synchronize()
+    return qd, kd, vd, o, lse
+
+
+def _check_rows(w, q, k, v, o, lse, rows, label, q_chunk_offset=0):
+    ridx = torch.as_tensor(rows, device=o.device)
+    o_s = to_np(o[:, ridx])
+    l_s = to_np(lse[:, :, ridx])
+    assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, q_chunk_offset, w.window_chunks, w.scale, rows=rows)
+    return compare(o_s, l_s, o_ref, l_ref, label=f"{label} ({len(rows)} rows)")
+
+
+def test_tiny_all_rows(dev):
+    w = WORKLOADS["tiny"]
+    _announce("tiny B=1 H=2 d=64 N=1024 L=256")
+    q, k, v = make_sequence(w)
+    _, _, _, o, lse = _full_call(w, q, k, v, dev)
+    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
+    compare(to_np(o), to_np(lse), o_ref, l_ref, label="tiny (all rows)")
+
+
+def test_480p_sampled(dev):
+    w = WORKLOADS["480p"]
+    _announce("480p B=1 H=12 d=128 N=18720 L=3120")
+    q, k, v = make_sequence(w)
+    _, _, _, o, lse = _full_call(w, q, k, v, dev)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=1024, seed=2)
+    _check_rows(w, q, k, v, o, lse, rows, "480p")
+
+
+def test_1080p_full_and_streaming_step(dev):
+    w = WORKLOADS["1080p"]
+    ws = WORKLOADS["1080p_stream"]
+    _announce("1080p B=1 H=12 d=128 N=65280 L=16320 + streaming step chunk 3")
+    q, k, v = make_sequence(w)
+    qd, kd, vd, o, lse = _full_call(w, q, k, v, dev)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=256, seed=3, band=0)
+    _check_rows(w, q, k, v, o, lse, rows, "1080p")
+
+    # streaming step: cache holds chunks 0-2, append chunk 3, attend chunk 3
+    sv = streaming_views(ws, qd, kd, vd)
+    cap = sv["n_kv"]
+    kc = torch.empty((w.B, cap, w.H, w.d), dtype=torch.bfloat16, device=dev)
+    vc = torch.empty_like(kc)
+    kc[:, :sv["cache_len"]].copy_(sv["k_prefix"])
+    vc[:, :sv["cache_len"]].copy_(sv["v_prefix"])
+    n_kv = fastvr.kv_cache_append(kc, vc, sv["k_new"].contiguous(), sv["v_new"].contiguous(), sv["cache_len"])
+    assert n_kv == cap
+    so, sl = fastvr.chunk_attn(sv["q_new"].contiguous(), kc, vc, chunk_len=ws.chunk_len,
+                               q_chunk_offset=sv["q_chunk_offset"], window_chunks=ws.window_chunks, scale=ws.scale)
+    torch.cuda.synchronize()
+    lo = sv["cache_len"]
+    assert torch.equal(kc, kd) and torch.equal(vc, vd)
+    assert torch.equal(so, o[:, lo:lo + so.shape[1]]), "streaming step differs from the parallel call"
+    assert torch.equal(sl, lse[:, :, lo:lo + so.shape[1]])
+    srows = sample_rows(so.shape[1], ws.chunk_len, n_random=128, seed=4, band=0)
+    _check_rows(ws, q[:, lo:lo + so.shape[1]], k, v, so, sl, srows, "1080p streaming step",
+                q_chunk_offset=sv["q_chunk_offset"])
+
+
+def test_wide_sliding_window_sampled(dev):
+    w = WORKLOADS["wide_sw"]
+    _announce("wide_sw B=1 H=24 d=128 N=138720 L=16320 W=2 outliers")
+    q, k, v = make_sequence(w)
+    _, _, _, o, lse = _full_call(w, q, k, v, dev)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=128, seed=5, band=0, tile=1024)
+    _check_rows(w, q, k, v, o, lse, rows, "wide_sw")
