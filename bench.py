@@ -108,7 +108,6 @@ def main():
     o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
 
-    calls = [("full", qd, kd, vd, o, lse, 0, w.n_tokens, w.n_tokens)]
     stream = args.workload == "1080p"
     if stream:
         ws = WORKLOADS["1080p_stream"]

@@ -121,6 +121,10 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
   if ((s = check_view({"k", k, k_sb, k_st, Nkv, 2}, B, hd, &kb)) != FASTVR_OK) return s;
   if ((s = check_view({"v", v, v_sb, v_st, Nkv, 2}, B, hd, &vb)) != FASTVR_OK) return s;
   if ((s = check_view({"o", o, o_sb, o_st, Nq, 4}, B, hd, &ob)) != FASTVR_OK) return s;
+  if (q_st >= fastvr::kMaxTokenStride || k_st >= fastvr::kMaxTokenStride || v_st >= fastvr::kMaxTokenStride ||
+      o_st >= fastvr::kMaxTokenStride)
+    return fail(FASTVR_ERR_UNSUPPORTED, "token strides must be below %lld elements",
+                (long long)fastvr::kMaxTokenStride);
   int64_t lb = 0;
   if (lse != nullptr) {
     if (!aligned(lse, 4)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse is not 4-byte aligned");

@@ -33,6 +33,8 @@ struct FwdGrid {
 constexpr int kFwdThreads = 512;  // 8 wave64 per workgroup
 constexpr int kFwdRowsPerItem = 256;
 constexpr int64_t kMaxFwdItems = (int64_t(1) << 32) / kFwdThreads - 1;
+// 32-bit buffer offsets of a 256-row tile: token strides stay below 2^22 elements
+constexpr int64_t kMaxTokenStride = int64_t(1) << 22;
 
 FwdGrid fwd_grid(int64_t B, int64_t H, int64_t nq, int64_t chunk_len);
 hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream);
