@@ -9,35 +9,33 @@
 //
 // Work decomposition: one workgroup (8 wave64, 512 threads) per
 // (batch, head, query chunk, 256-row query tile); tiles never straddle a chunk.
-// Each wave owns 32 query rows; two waves share each SIMD.  Scores are computed
-// transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the accumulator puts
-// one query per lane (column) and 16 keys per lane (rows), so row max and row
-// sum are in-lane plus one exchange between the two 32-lane halves.  The same
-// registers, rounded to bf16, are the B operand of O^T = V^T P^T; V is staged
-// transposed in LDS with its keys permuted so that every A-operand read is one
-// 16-byte LDS load.
+// Each wave owns 32 query rows.  Scores are computed transposed,
+// S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the accumulator puts one query per
+// lane (column) and 16 keys per lane (rows), so row max and row sum are in-lane
+// plus one exchange between the two 32-lane halves.  The same registers,
+// rounded to bf16, are the B operand of O^T = V^T P^T.
 //
-// Memory: buffer loads with per-tile descriptors (out-of-range rows read as
-// zero, no per-lane bounds checks); K tiles go straight from HBM into
-// XOR-swizzled LDS (buffer_load ... lds); V tiles pass through registers for
-// the 4x4 transpose.  K and V^T tiles of 64 keys are double-buffered.
+// Matrix-core / vector-ALU ping-pong: waves 0-3 (group A) and 4-7 (group B)
+// share the four SIMDs one-to-one.  Time is cut into slots separated by
+// workgroup barriers; in every slot one group runs only MFMAs (scores of tile
+// j and P.V of tile j-1) while the other runs only the online softmax of its
+// last scores, and the roles swap each slot.  Each SIMD therefore always has a
+// matrix-core wave and a vector-ALU wave side by side.
 //
-// Pipeline per KV tile j (one barrier per tile):
-//   phase A: MFMA  S(j+1) = K(j+1) Q^T          | VALU  P(j) = exp2(t(j)), bf16 pack, half of rowsum
-//   (rare)  rescale O by alpha(j) if any row's running maximum grew
-//   phase B: MFMA  O^T += V(j)^T P(j)^T          | VALU  rest of rowsum, max of S(j+1), t(j+1) = S*c - m
-// with t = s * scale * log2(e) - m (log2 domain, exact running maximum m).
+// Memory: all K and V tiles (64 keys) travel by DMA straight from HBM into LDS
+// (buffer_load ... lds, per-tile buffer descriptors: rows outside the visible
+// interval read as zero), triple-buffered and issued two tiles ahead.  K is
+// stored chunk-major (16-byte chunk c of key row r at (c * 64 + r) * 16), V
+// row-major with the 16-byte chunk index XOR 2*(row & 3); V^T operands are read
+// with ds_read_b64_tr_b16, which transposes 4x16 blocks across 16 lanes.
+// Both layouts are free of LDS bank conflicts for the operand reads.
+//
+// Online softmax in the log2 domain: t = s * scale * log2(e), exact running
+// maximum m, running sum l; O is rescaled only when a row's maximum grows.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "launch.h"
-
-#ifndef FASTVR_SETPRIO
-#define FASTVR_SETPRIO 0
-#endif
-#ifndef FASTVR_SCHED
-#define FASTVR_SCHED 0
-#endif
 
 namespace fastvr {
 namespace {
@@ -47,13 +45,20 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = kFwdThreads / 64;  // 8
 constexpr int kBQ = 32 * kWaves;          // 256 query rows per workgroup
 constexpr int kBK = 64;                   // keys per KV tile
+constexpr int kStages = 3;                // LDS buffers per operand
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kBufFlags = 0x00020000;     // raw buffer, 32-bit data format (gfx9 family)
+#ifndef FASTVR_SCHED
+#define FASTVR_SCHED 1
+#endif
 static_assert(kBQ == kFwdRowsPerItem, "tile height mismatch");
 
 struct Params {
@@ -79,7 +84,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, kBufFlags);
 }
 
-// value of the other 32-lane half of the wave, combined with this lane's
+// this lane's value and the value of the same lane in the other 32-lane half
 __device__ __forceinline__ float swap_halves(float x, float* other) {
   const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x), __builtin_bit_cast(uint32_t, x),
                                                   false, false);
@@ -87,40 +92,55 @@ __device__ __forceinline__ float swap_halves(float x, float* other) {
   return __builtin_bit_cast(float, (uint32_t)r[0]);
 }
 
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource (V#) of `bytes` bytes at `base`: stride 0, raw addressing,
+// 32-bit data format.  Reads at offsets >= bytes return zero.
+__device__ __forceinline__ i32x4 make_vsharp(const void* base, int64_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  const int n = bytes > 0x7fffffff ? 0x7fffffff : (int)bytes;
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffff), n, kBufFlags};
+}
+
+// One 16-byte-per-lane DMA from a buffer straight into LDS at lds_addr + 16 * lane
+// (buffer_load_dwordx4 ... lds).  Issued as inline assembly on purpose: the
+// compiler then does not pair every later LDS read with a wait for all
+// outstanding DMA; completion is ordered explicitly with counted vmcnt waits
+// followed by a workgroup barrier.  M0 carries the LDS address and is not used
+// by any other instruction of this kernel.
+__device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 rsrc, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Workgroup barrier with LDS visibility; vector-memory (DMA) completion is
+// handled separately with counted waits so that prefetches stay in flight.
+__device__ __forceinline__ void barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// s_waitcnt vmcnt(N): every DMA issued by this wave except the newest N
+// instructions has landed (inline assembly, so the compiler cannot relax it)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt();
+template <>
+__device__ __forceinline__ void wait_vmcnt<0>() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+template <>
+__device__ __forceinline__ void wait_vmcnt<2>() { asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); }
+template <>
+__device__ __forceinline__ void wait_vmcnt<4>() { asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); }
+
 // instruction-group ordering hints for the scheduler (sched_group_barrier masks)
-#define FASTVR_SCHED_VALU 0x002
-#define FASTVR_SCHED_MFMA 0x008
-#define FASTVR_SCHED_DS_READ 0x100
-#if FASTVR_SCHED
-#define SCHED(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
-#else
-#define SCHED(mask, n) ((void)0)
-#endif
-#if FASTVR_SETPRIO
-#define SETPRIO(p) __builtin_amdgcn_s_setprio(p)
-#else
-#define SETPRIO(p) ((void)0)
-#endif
-
-// ---------------------------------------------------------------------------
-// LDS layouts
-//   K tile   [D/8 chunks][kBK rows][8] bf16: 16-byte chunk c of key row r at
-//            (c * kBK + r) * 16 bytes, so lanes reading consecutive rows of one
-//            chunk touch consecutive 16-byte slots (no bank conflicts) and a lane's
-//            reads for different chunks differ by compile-time offsets
-//   V^T tile [D rows][kBK]   bf16, key order permuted inside each group of 16
-//            (swap of key bits 2 and 3), 16-byte chunk index XOR vswz(d)
-// ---------------------------------------------------------------------------
-template <int D>
-struct Lds {
-  static constexpr int kKStage = kBK * D;
-  static constexpr int kVStage = D * kBK;
-  static constexpr int kElems = 2 * kKStage + 2 * kVStage;
-  static __device__ __forceinline__ int k_off(int row, int chunk) { return (chunk * kBK + row) * 8; }
-};
-
-__device__ __forceinline__ int vswz(int d) { return (d & 7) ^ ((d >> 3) & 1); }
-__device__ __forceinline__ int vt_off(int d, int chunk) { return d * kBK + ((chunk ^ vswz(d)) << 3); }
+#define SCHED_MFMA 0x008
+#define SCHED_DS_READ 0x100
 
 // blockIdx -> (local query chunk, batch*head, tile).  Workgroups are handed to
 // the 8 XCDs round-robin; within each full round of 256 workgroups the
@@ -153,128 +173,125 @@ __device__ __forceinline__ void decode_item(const Params& p, int i, int& cl, int
   }
 }
 
-// s_waitcnt vmcnt(0) (gfx9 encoding, other counters left at their maximum):
-// direct-to-LDS loads must have landed before the barrier that publishes them.
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
 template <int D, bool NEG>
 struct Attn {
-  static constexpr int kKPer = kBK * (D / 8) / kFwdThreads;  // 16-byte K chunks per thread per tile
-  static constexpr int kVBlocks = (kBK / 4) * (D / 4);       // 4x4 V blocks per tile
+  static constexpr int kChunks = D / 8;                        // 16-byte chunks per key row
+  static constexpr int kStage = kBK * D;                       // bf16 elements per stage (K or V)
+  static constexpr int kDmaPer = kBK * kChunks / kFwdThreads;  // DMA instructions per wave per operand
+  static constexpr int kLdsElems = 2 * kStages * kStage;
+  static_assert(kDmaPer >= 1 && kChunks >= 8, "head_dim must be 64 or 128");
 
-  // geometry
-  int tid, lane, wave, n, hh;
-  int lo, hi;  // visible key interval [lo, hi)
-  int n_tiles;
+  int lane, wave, n, hh;
+  int lo, hi, n_tiles;
   float c;
-  uint16_t* ks;  // K stages
-  uint16_t* vt;  // V^T stages
+  uint16_t* ks;  // K stages (chunk-major)
+  uint16_t* vs;  // V stages (row-major, swizzled)
   const uint16_t* kb;
   const uint16_t* vb;
   int k_st, v_st;
-  // per-lane constant offsets
-  uint32_t k_voff;  // byte offset of this lane's K row (+16 * chunk)
-  uint32_t v_voff;  // byte offset of this lane's first V row (+ e * row stride via soffset)
-  int vst_off[4];
-  int koff;         // element offset of this lane's K operand row, chunk hh
-  int voff[4];
-  // state
+  uint32_t k_dma_off, v_dma_off;  // per-lane byte offsets of this wave's DMA rows
+  int k_rd;                        // element offset of this lane's K operand reads
+  int v_rd[D / 32];                // byte offsets of this lane's V^T transpose reads
   u32x4 qf[D / 16];
   f32x16 o[D / 32];
-  f32x16 s[2];  // raw scores of the next tile
-  f32x16 t[2];  // current tile: s*c - m, then exp2 of it in place
-  u32x4 pf[4];  // bf16 P fragments of the current tile
-  u32x2 vr[4];  // V tile in flight (registers)
-  float m_run, l_run, alpha, psum;
+  f32x16 s[2];
+  u32x4 pf[4];
+  float m_run, l_run;
 
   __device__ __forceinline__ void init_offsets() {
-    // K: wave w, round i loads chunk c = i * 8 + w of all 64 rows; lane = row
-    k_voff = (uint32_t)(lane * k_st + wave * 8) * 2u;
-    // V: thread owns keys 4kq..4kq+3 x dims 4dq..4dq+3; in V^T those keys sit in
-    // 16-byte chunk `chunk`, 8-byte half `half` of rows 4dq..4dq+3
-    const int kq = tid & 15, dq = tid >> 4;
-    v_voff = (uint32_t)(kq * 4 * v_st + dq * 4) * 2u;
-    const int chunk = ((kq >> 2) << 1) | (kq & 1), half = (kq >> 1) & 1;
+    // K: DMA instruction i of wave w moves chunk c = i * 8 + w of all 64 rows; lane = row
+    k_dma_off = (uint32_t)(lane * k_st + wave * 8) * 2u;
+    // V: DMA instruction i of wave w fills LDS chunk slots (i * 8 + w) * 64 + lane
+    {
+      const int P = wave * 64 + lane;
+      const int row = P / kChunks, phys = P % kChunks;
+      const int logical = phys ^ (2 * (row & 3));
+      v_dma_off = (uint32_t)(row * v_st + logical * 8) * 2u;
+    }
+    // K operand (A of S^T = K Q^T): row mb*32 + n, chunk 2*kk + hh
+    k_rd = (hh * kBK + n) * 8;
+    // V^T operand via transpose reads: 16-lane block b = lane / 16 reads rows
+    // hh*4 + (i >> 2) (+ 16 g + 8 rho), dims dm*32 + 16*(b & 1) + 4*(i & 3) .. + 3
+    const int i = lane & 15, b = lane >> 4;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) vst_off[x] = vt_off(dq * 4 + x, chunk) + half * 4;
-    koff = Lds<D>::k_off(n, hh);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) voff[g] = vt_off(n, 2 * g + hh);
-  }
-
-  // K tile j -> LDS stage (direct buffer -> LDS, rows >= hi read as zero)
-  __device__ __forceinline__ void load_k(int j, int stage) {
-    const int t0 = lo + j * kBK;
-    const int rows = (hi - t0 < kBK) ? hi - t0 : kBK;
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(kb + (int64_t)t0 * k_st, (int64_t)rows * k_st * 2);
-#pragma unroll
-    for (int i = 0; i < kKPer; ++i) {
-      const int c = i * kWaves + wave;
-      uint16_t* dst = ks + stage * Lds<D>::kKStage + c * kBK * 8;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, k_voff, i * kWaves * 16, 0, 0);
+    for (int dm = 0; dm < D / 32; ++dm) {
+      const int row = hh * 4 + (i >> 2);
+      const int logical = dm * 4 + 2 * (b & 1) + ((i >> 1) & 1);
+      const int phys = logical ^ (2 * (row & 3));
+      v_rd[dm] = row * (D * 2) + phys * 16 + (i & 1) * 8;
     }
   }
 
-  // V tile j -> registers (rows >= hi read as zero)
-  __device__ __forceinline__ void load_v(int j) {
-    if (tid < kVBlocks) {
-      const int t0 = lo + j * kBK;
-      const int rows = (hi - t0 < kBK) ? hi - t0 : kBK;
-      const __amdgpu_buffer_rsrc_t r = make_rsrc(vb + (int64_t)t0 * v_st, (int64_t)rows * v_st * 2);
+  // DMA of one K (or V) tile: `base` points at the tile's first key row, `rows`
+  // valid rows (0 past the end of the interval: the stage is filled with zeros).
+  __device__ __forceinline__ void dma_k(const uint16_t* base, int rows, int stage) {
+    const i32x4 r = make_vsharp(base, (int64_t)rows * k_st * 2);
+    const uint32_t st = lds_addr(ks + stage * kStage);
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        vr[e] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, v_voff, e * v_st * 2, 0));
+    for (int i = 0; i < kDmaPer; ++i) {
+      const int ch = i * kWaves + wave;
+      dma16(__builtin_amdgcn_readfirstlane(st + ch * kBK * 16), k_dma_off, r, i * kWaves * 16);
     }
   }
-
-  // registers -> transposed V^T stage: row 4dq+x gets keys 4kq..4kq+3 of dim x
-  __device__ __forceinline__ void store_v(int stage) {
-    if (tid < kVBlocks) {
-      uint16_t* base = vt + stage * Lds<D>::kVStage;
+  __device__ __forceinline__ void dma_v(const uint16_t* base, int rows, int stage) {
+    const i32x4 r = make_vsharp(base, (int64_t)rows * v_st * 2);
+    const uint32_t st = lds_addr(vs + stage * kStage);
+    constexpr int kRowsPerInst = 64 / kChunks;  // rows covered by one wave instruction
 #pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const uint32_t w0 = (x < 2) ? vr[0].x : vr[0].y, w1 = (x < 2) ? vr[1].x : vr[1].y;
-        const uint32_t w2 = (x < 2) ? vr[2].x : vr[2].y, w3 = (x < 2) ? vr[3].x : vr[3].y;
-        const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;  // high or low bf16 of each word
-        u32x2 out;
-        out.x = __builtin_amdgcn_perm(w1, w0, sel);
-        out.y = __builtin_amdgcn_perm(w3, w2, sel);
-        *reinterpret_cast<u32x2*>(base + vst_off[x]) = out;
-      }
+    for (int i = 0; i < kDmaPer; ++i) {
+      const int slot0 = (i * kWaves + wave) * 64;
+      dma16(__builtin_amdgcn_readfirstlane(st + slot0 * 16), v_dma_off, r, i * kWaves * kRowsPerInst * v_st * 2);
     }
   }
+  __device__ __forceinline__ int tile_rows(int j) const {
+    const int r = hi - (lo + j * kBK);
+    return r <= 0 ? 0 : (r < kBK ? r : kBK);
+  }
 
-  // S^T(tile in stage) = K Q^T : 16 MFMAs, raw scores land in s[]
-  __device__ __forceinline__ void qk(int stage) {
-    const uint16_t* kst = ks + stage * Lds<D>::kKStage;
+  // One matrix-core slot: S^T(tile in st_k) = K Q^T (QK) and/or
+  // O^T += V^T P^T (tile in st_v, PV).  The QK and PV MFMAs are interleaved
+  // (six independent accumulators) and the LDS operand reads run kAhead MFMA
+  // pairs ahead.  K fragments: one 16-byte read; V^T fragments: two transpose
+  // reads of 4 keys each.
+  template <bool QK, bool PV>
+  __device__ __forceinline__ void mfma_slot(int st_k, int st_v) {
+    constexpr int kN = D / 8;  // MFMAs of each kind (QK: D/16 x 2 key blocks; PV: 4 key groups x D/32)
+    constexpr int kAhead = 3;
+    constexpr int kReads = (QK ? 1 : 0) + (PV ? 2 : 0);
+    constexpr int kMfma = (QK ? 1 : 0) + (PV ? 1 : 0);
+    const uint16_t* kst = ks + st_k * kStage + k_rd;
+    const char* vst = reinterpret_cast<const char*>(vs + st_v * kStage);
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + koff + Lds<D>::k_off(mb * 32, 2 * kk));
+    for (int i = 0; i < kN; ++i) {
+      if (QK) {
+        const int kk = i >> 1, mb = i & 1;
+        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + ((2 * kk) * kBK + mb * 32) * 8);
         s[mb] = (kk == 0) ? mfma32(a, qf[kk], f32x16{}) : mfma32(a, qf[kk], s[mb]);
       }
-    }
-  }
-
-  // O^T += V^T P^T : 16 MFMAs
-  __device__ __forceinline__ void pv(int stage) {
-    const uint16_t* vst = vt + stage * Lds<D>::kVStage;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-#pragma unroll
-      for (int dm = 0; dm < D / 32; ++dm) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(vst + voff[g] + dm * 32 * kBK);
-        o[dm] = mfma32(a, pf[g], o[dm]);
+      if (PV) {
+        const int g = i / (D / 32), dm = i % (D / 32);
+        const char* base = vst + v_rd[dm] + g * 16 * (D * 2);
+        const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
+        const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * (D * 2)));
+        const i16x8 a8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[dm] = mfma32(__builtin_bit_cast(u32x4, a8), pf[g], o[dm]);
       }
     }
+#if FASTVR_SCHED
+    __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kAhead * kReads, 0);
+#pragma unroll
+    for (int i = 0; i < kN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, kMfma, 0);
+      if (i + kAhead < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kReads, 0);
+    }
+#endif
   }
 
-  // Row maximum of the raw scores in s[] (MASK: keys at tile positions >= n_valid
-  // are outside the visible interval), new running maximum, alpha = 2^(m_old - m_new)
-  // and t = s*c - m_new (-inf for masked keys).
+  // Online softmax of the scores in s[] (MASK: keys at tile positions >= n_valid
+  // lie outside the visible interval): new running maximum, rescale of O and l,
+  // P = exp2(s*c - m) rounded to bf16 fragments, running sum from the fp32 P.
   template <bool MASK>
-  __device__ __forceinline__ void row_max_and_shift(int n_valid) {
+  __device__ __forceinline__ void softmax(int n_valid) {
     constexpr float kInf = __builtin_inff();
     float mx = NEG ? kInf : -kInf;
 #pragma unroll
@@ -292,113 +309,58 @@ struct Attn {
     const float mine = swap_halves(mx, &other);
     mx = NEG ? __builtin_fminf(mine, other) : __builtin_fmaxf(mine, other);
     const float m_new = __builtin_fmaxf(m_run, mx * c);
-    alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
     m_run = m_new;
     const float nm = -m_new;
+    float psum = 0.f;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float x = __builtin_fmaf(s[mb][v], c, nm);
+        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][v], c, nm));
         if (MASK) {
           const int key = mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          x = (key < n_valid) ? x : -kInf;
+          p = (key < n_valid) ? p : 0.f;
         }
-        t[mb][v] = x;
+        s[mb][v] = p;
+        psum += p;
       }
-  }
-
-  // P = exp2(t) in place, bf16 fragments, first half of the row sum
-  __device__ __forceinline__ void exp_and_pack() {
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) t[mb][v] = __builtin_amdgcn_exp2f(t[mb][v]);
+    l_run = l_run * alpha + psum;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       bf16x8 b;
 #pragma unroll
-      for (int r = 0; r < 8; ++r) b[r] = (__bf16)t[g >> 1][8 * (g & 1) + r];
+      for (int r = 0; r < 8; ++r) b[r] = (__bf16)s[g >> 1][8 * (g & 1) + r];
       pf[g] = __builtin_bit_cast(u32x4, b);
     }
-    float ps = 0.f;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) ps += t[0][v];
-    psum = ps;
-  }
-
-  __device__ __forceinline__ void finish_sum() {
-    float ps = psum;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) ps += t[1][v];
-    l_run = l_run * alpha + ps;
-  }
-
-  __device__ __forceinline__ void rescale_o() {
     if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
 #pragma unroll
       for (int dm = 0; dm < D / 32; ++dm) o[dm] *= alpha;
     }
   }
 
-  __device__ __forceinline__ void sched_phase() {
-    // 16 MFMAs, each followed by ~4 VALU ops; LDS operand reads run 4 ahead
-    SCHED(FASTVR_SCHED_DS_READ, 4);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      SCHED(FASTVR_SCHED_MFMA, 1);
-      SCHED(FASTVR_SCHED_VALU, 4);
-      if (i < 12) SCHED(FASTVR_SCHED_DS_READ, 1);
-    }
-  }
-
-  // one pipelined KV tile: j in [0, n_tiles - 2]; t[] holds tile j, s[] receives tile j+1
-  template <bool MASK_NEXT>
-  __device__ __forceinline__ void step(int j, int n_valid_next) {
-    const int cur = j & 1, nxt = (j + 1) & 1;
-    load_v(j + 1);
-    if (j + 2 < n_tiles) load_k(j + 2, cur);
-    // phase A: scores of tile j+1 on the matrix cores, exp2 of tile j on the VALU
-    SETPRIO(1);
-    qk(nxt);
-    exp_and_pack();
-    sched_phase();
-    SETPRIO(0);
-    rescale_o();
-    // phase B: O += P V on the matrix cores, row statistics of tile j+1 on the VALU
-    SETPRIO(1);
-    pv(cur);
-    finish_sum();
-    row_max_and_shift<MASK_NEXT>(n_valid_next);
-    sched_phase();
-    SETPRIO(0);
-    store_v(nxt);
-    wait_vmem();
-    __syncthreads();
-  }
-
-  // same loads, stores and barriers as step() for a wave whose rows are all padding
-  __device__ __forceinline__ void step_idle(int j) {
-    load_v(j + 1);
-    if (j + 2 < n_tiles) load_k(j + 2, j & 1);
-    store_v((j + 1) & 1);
-    wait_vmem();
-    __syncthreads();
+  __device__ __forceinline__ void softmax_last(int last_valid) {
+    if (last_valid < kBK)
+      softmax<true>(last_valid);
+    else
+      softmax<false>(kBK);
   }
 };
 
 template <int D, bool NEG>
 __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Params p) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[Lds<D>::kElems];
-  Attn<D, NEG> a;
+  using A = Attn<D, NEG>;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[A::kLdsElems];
+  A a;
   a.ks = smem;
-  a.vt = smem + 2 * Lds<D>::kKStage;
-  a.tid = threadIdx.x;
-  a.lane = a.tid & 63;
-  a.wave = a.tid >> 6;
+  a.vs = smem + kStages * A::kStage;
+  const int tid = threadIdx.x;
+  a.lane = tid & 63;
+  a.wave = tid >> 6;
   a.n = a.lane & 31;
   a.hh = a.lane >> 5;
   a.c = p.c;
+  const int group = a.wave >> 2;  // 0: waves 0-3, 1: waves 4-7 (one wave of each per SIMD)
 
   int cl, bh, t;
   decode_item(p, blockIdx.x, cl, bh, t);
@@ -420,12 +382,14 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
 
   const int row = q0 + a.wave * 32 + a.n;
   const bool active = (q0 + a.wave * 32) < q_end;  // wave-uniform
-  const int last_valid = a.hi - (a.lo + (a.n_tiles - 1) * kBK);  // keys in the last tile
+  const int n = a.n_tiles;
+  const int last_valid = a.hi - (a.lo + (n - 1) * kBK);  // keys in the last tile
 
-  // prologue: V(0) to registers, K(0), K(1) to LDS, Q fragments
-  a.load_v(0);
-  a.load_k(0, 0);
-  if (a.n_tiles > 1) a.load_k(1, 1);
+  // prologue: K(0), K(1), V(0) to LDS, Q fragments to registers
+  const int64_t k_step = (int64_t)kBK * a.k_st, v_step = (int64_t)kBK * a.v_st;
+  a.dma_k(a.kb + (int64_t)a.lo * a.k_st, a.tile_rows(0), 0);
+  a.dma_k(a.kb + (int64_t)a.lo * a.k_st + k_step, a.tile_rows(1), 1);
+  a.dma_v(a.vb + (int64_t)a.lo * a.v_st, a.tile_rows(0), 0);
   {
     const int rows = (q_end - q0 < kBQ) ? q_end - q0 : kBQ;
     const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (int64_t)b * p.q_sb + (int64_t)q0 * p.q_st + (int64_t)h * D,
@@ -440,41 +404,99 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   for (int dm = 0; dm < D / 32; ++dm) a.o[dm] = f32x16{};
   a.m_run = -__builtin_inff();
   a.l_run = 0.f;
-  a.store_v(0);
-  wait_vmem();
-  __syncthreads();
+  wait_vmcnt<0>();
+  // the same wait through the builtin, so the compiler's own bookkeeping also
+  // sees the Q loads complete and inserts no further vmcnt waits for them
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  barrier();
+  constexpr int kBatch = 2 * A::kDmaPer;  // DMA instructions per wave per batch (one K and one V tile)
 
+  // Slot 2j: group A runs MFMA(j) = S(j) and P(j-1).V(j-1); group B the softmax of tile j-1.
+  // Slot 2j+1: group A the softmax of tile j; group B MFMA(j).
+  // Before slot 2j the DMA of K(j+2) and V(j+1) is issued (zeros past the end); the
+  // barrier closing slot 2j+1 waits for the batch issued two slots earlier.  Tile j
+  // lives in LDS stage j % 3, so K(j+2) reuses the stage of tile j-1 and V(j+1)
+  // the third one.  The first tile, the last tile (the only one that can be
+  // ragged) and the drain (j = n) are peeled out of the loop.
+  const uint16_t* k_next = a.kb + (int64_t)a.lo * a.k_st + 2 * k_step;  // K(j+2)
+  const uint16_t* v_next = a.vb + (int64_t)a.lo * a.v_st + v_step;      // V(j+1)
+  int st_cur = 0, st_prev = 2, st_next = 1;  // stages of tiles j, j-1 (== j+2) and j+1
+  // j = 0
+  a.dma_k(k_next, a.tile_rows(2), st_prev);
+  a.dma_v(v_next, a.tile_rows(1), st_next);
+  k_next += k_step;
+  v_next += v_step;
+  if (active && group == 0) a.template mfma_slot<true, false>(st_cur, 0);
+  barrier();
   if (active) {
-    a.qk(0);
-    if (a.n_tiles == 1 && last_valid < kBK)
-      a.template row_max_and_shift<true>(last_valid);
-    else
-      a.template row_max_and_shift<false>(kBK);
+    if (group == 0) {
+      if (n == 1)
+        a.softmax_last(last_valid);
+      else
+        a.template softmax<false>(kBK);
+    } else {
+      a.template mfma_slot<true, false>(st_cur, 0);
+    }
   }
-  __syncthreads();  // every wave has read K stage 0 before it is refilled
-  for (int j = 0; j + 2 < a.n_tiles; ++j) {
-    if (active)
-      a.template step<false>(j, kBK);
-    else
-      a.step_idle(j);
+  wait_vmcnt<kBatch>();
+  barrier();
+  if (n >= 2) {
+    st_prev = st_cur;
+    st_cur = st_next;
+    st_next = (st_next == 2) ? 0 : st_next + 1;
+    for (int j = 1; j + 1 < n; ++j) {
+      a.dma_k(k_next, a.tile_rows(j + 2), st_prev);
+      a.dma_v(v_next, a.tile_rows(j + 1), st_next);
+      k_next += k_step;
+      v_next += v_step;
+      // ---- slot 2j ----
+      if (active) {
+        if (group == 0)
+          a.template mfma_slot<true, true>(st_cur, st_prev);
+        else
+          a.template softmax<false>(kBK);
+      }
+      barrier();
+      // ---- slot 2j+1 ----
+      if (active) {
+        if (group == 0)
+          a.template softmax<false>(kBK);
+        else
+          a.template mfma_slot<true, true>(st_cur, st_prev);
+      }
+      wait_vmcnt<kBatch>();
+      barrier();
+      st_prev = st_cur;
+      st_cur = st_next;
+      st_next = (st_next == 2) ? 0 : st_next + 1;
+    }
+    // j = n - 1: last tile (no further DMA)
+    if (active) {
+      if (group == 0)
+        a.template mfma_slot<true, true>(st_cur, st_prev);
+      else
+        a.template softmax<false>(kBK);
+    }
+    barrier();
+    if (active) {
+      if (group == 0)
+        a.softmax_last(last_valid);
+      else
+        a.template mfma_slot<true, true>(st_cur, st_prev);
+    }
   }
-  if (a.n_tiles >= 2) {
-    const int j = a.n_tiles - 2;
-    if (!active)
-      a.step_idle(j);
-    else if (last_valid < kBK)
-      a.template step<true>(j, last_valid);
+  wait_vmcnt<0>();
+  barrier();
+  // j = n: drain, P(n-1).V(n-1)
+  if (active) {
+    if (group == 0)
+      a.template mfma_slot<false, true>(0, st_cur);
     else
-      a.template step<false>(j, kBK);
+      a.softmax_last(last_valid);
   }
+  barrier();
+  if (active && group == 1) a.template mfma_slot<false, true>(0, st_cur);
   if (!active) return;
-
-  // last tile
-  const int jl = a.n_tiles - 1;
-  a.exp_and_pack();
-  a.rescale_o();
-  a.pv(jl & 1);
-  a.finish_sum();
 
   // epilogue: the two halves of the wave hold partial sums over disjoint keys
   float l_other;
