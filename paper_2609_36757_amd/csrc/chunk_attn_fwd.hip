@@ -24,11 +24,13 @@
 //
 // Memory: all K and V tiles (64 keys) travel by DMA straight from HBM into LDS
 // (buffer_load ... lds, per-tile buffer descriptors: rows outside the visible
-// interval read as zero), triple-buffered and issued two tiles ahead.  K is
-// stored chunk-major (16-byte chunk c of key row r at (c * 64 + r) * 16), V
-// row-major with the 16-byte chunk index XOR 2*(row & 3); V^T operands are read
-// with ds_read_b64_tr_b16, which transposes 4x16 blocks across 16 lanes.
-// Both layouts are free of LDS bank conflicts for the operand reads.
+// interval read as zero), triple-buffered and issued two tiles ahead, K in the
+// even slots and V in the odd ones.  Both tiles are stored row-major, K with
+// its 16-byte chunk index XOR (row & 15), V with it XOR vswz(row & 3), so one
+// DMA instruction moves four whole key rows; V^T operands are read with
+// ds_read_b64_tr_b16, which transposes 4x16 blocks across 16 lanes.
+// Both layouts keep the operand reads free of LDS bank conflicts (64 banks,
+// 32 lanes served per cycle).
 //
 // Online softmax in the log2 domain: t = s * scale * log2(e), exact running
 // maximum m, running sum l; O is rescaled only when a row's maximum grows.
@@ -58,6 +60,15 @@ constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kBufFlags = 0x00020000;     // raw buffer, 32-bit data format (gfx9 family)
 #ifndef FASTVR_SCHED
 #define FASTVR_SCHED 1
+#endif
+#ifndef FASTVR_PRIO
+#define FASTVR_PRIO 0
+#endif
+#ifndef FASTVR_AHEAD
+#define FASTVR_AHEAD 3
+#endif
+#ifndef FASTVR_DMA_SPLIT
+#define FASTVR_DMA_SPLIT 0
 #endif
 static_assert(kBQ == kFwdRowsPerItem, "tile height mismatch");
 
@@ -109,6 +120,13 @@ __device__ __forceinline__ i32x4 make_vsharp(const void* base, int64_t bytes) {
 // followed by a workgroup barrier.  M0 carries the LDS address and is not used
 // by any other instruction of this kernel.
 __device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 rsrc, int soff) {
+  // every scalar operand is wave-uniform; readfirstlane pins it to SGPRs
+  rsrc.x = __builtin_amdgcn_readfirstlane(rsrc.x);
+  rsrc.y = __builtin_amdgcn_readfirstlane(rsrc.y);
+  rsrc.z = __builtin_amdgcn_readfirstlane(rsrc.z);
+  rsrc.w = __builtin_amdgcn_readfirstlane(rsrc.w);
+  soff = __builtin_amdgcn_readfirstlane(soff);
+  lds_addr = __builtin_amdgcn_readfirstlane(lds_addr);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
                : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
@@ -125,6 +143,16 @@ __device__ __forceinline__ void barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// XOR applied to the 16-byte chunk index of V row r (u = r & 3).  A transpose
+// read by lanes 0-31 touches rows u = 0..3 and the chunks 4*dm + (0..3); the
+// pattern 0, 6, 12, 10 spreads those 16 chunks over all 64 banks (and any 16
+// lanes over 8 distinct chunk slots).  With 8 chunks per row (head_dim 64) the
+// pattern 2u keeps them within the row.
+template <int D>
+__device__ __forceinline__ int vswz(int u) {
+  return D >= 128 ? (((u & 1) * 6) ^ ((u >> 1) * 12)) : 2 * u;
 }
 
 // s_waitcnt vmcnt(N): every DMA issued by this wave except the newest N
@@ -177,7 +205,10 @@ template <int D, bool NEG>
 struct Attn {
   static constexpr int kChunks = D / 8;                        // 16-byte chunks per key row
   static constexpr int kStage = kBK * D;                       // bf16 elements per stage (K or V)
-  static constexpr int kDmaPer = kBK * kChunks / kFwdThreads;  // DMA instructions per wave per operand
+  // Waves issuing the DMA of one tile: all 8, or (split) the 4 waves that run
+  // the softmax in that slot, each with twice the instructions.
+  static constexpr int kDmaWaves = FASTVR_DMA_SPLIT ? kWaves / 2 : kWaves;
+  static constexpr int kDmaPer = kBK * kChunks / (64 * kDmaWaves);  // DMA instructions per issuing wave per tile
   static constexpr int kLdsElems = 2 * kStages * kStage;
   static_assert(kDmaPer >= 1 && kChunks >= 8, "head_dim must be 64 or 128");
 
@@ -190,7 +221,7 @@ struct Attn {
   const uint16_t* vb;
   int k_st, v_st;
   uint32_t k_dma_off, v_dma_off;  // per-lane byte offsets of this wave's DMA rows
-  int k_rd;                        // element offset of this lane's K operand reads
+  int k_rd[D / 16];                // byte offsets of this lane's K operand reads (row n, chunk 2kk + hh)
   int v_rd[D / 32];                // byte offsets of this lane's V^T transpose reads
   u32x4 qf[D / 16];
   f32x16 o[D / 32];
@@ -198,18 +229,23 @@ struct Attn {
   u32x4 pf[4];
   float m_run, l_run;
 
+  // XOR applied to the 16-byte chunk index of K row r: 16 consecutive rows read
+  // the same logical chunk from 16 distinct bank groups
+  static __device__ __forceinline__ int kswz(int row) { return row & (kChunks - 1) & 15; }
+
   __device__ __forceinline__ void init_offsets() {
-    // K: DMA instruction i of wave w moves chunk c = i * 8 + w of all 64 rows; lane = row
-    k_dma_off = (uint32_t)(lane * k_st + wave * 8) * 2u;
-    // V: DMA instruction i of wave w fills LDS chunk slots (i * 8 + w) * 64 + lane
+    // DMA instruction i of wave w fills LDS chunk slots (i * 8 + w) * 64 + lane of
+    // a stage: row P / kChunks, physical chunk P % kChunks.  The row offset i * 8 * 64
+    // / kChunks goes into the scalar offset; row & 15 does not depend on i.
     {
-      const int P = wave * 64 + lane;
+      const int P = (wave % kDmaWaves) * 64 + lane;
       const int row = P / kChunks, phys = P % kChunks;
-      const int logical = phys ^ (2 * (row & 3));
-      v_dma_off = (uint32_t)(row * v_st + logical * 8) * 2u;
+      k_dma_off = (uint32_t)(row * k_st + (phys ^ kswz(row)) * 8) * 2u;
+      v_dma_off = (uint32_t)(row * v_st + (phys ^ vswz<D>(row & 3)) * 8) * 2u;
     }
-    // K operand (A of S^T = K Q^T): row mb*32 + n, chunk 2*kk + hh
-    k_rd = (hh * kBK + n) * 8;
+    // K operand (A of S^T = K Q^T): row mb*32 + n, chunk 2*kk + hh (mb adds 32 rows)
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) k_rd[kk] = n * (D * 2) + (((2 * kk + hh) ^ kswz(n)) * 16);
     // V^T operand via transpose reads: 16-lane block b = lane / 16 reads rows
     // hh*4 + (i >> 2) (+ 16 g + 8 rho), dims dm*32 + 16*(b & 1) + 4*(i & 3) .. + 3
     const int i = lane & 15, b = lane >> 4;
@@ -217,7 +253,7 @@ struct Attn {
     for (int dm = 0; dm < D / 32; ++dm) {
       const int row = hh * 4 + (i >> 2);
       const int logical = dm * 4 + 2 * (b & 1) + ((i >> 1) & 1);
-      const int phys = logical ^ (2 * (row & 3));
+      const int phys = logical ^ vswz<D>(row & 3);
       v_rd[dm] = row * (D * 2) + phys * 16 + (i & 1) * 8;
     }
   }
@@ -227,10 +263,11 @@ struct Attn {
   __device__ __forceinline__ void dma_k(const uint16_t* base, int rows, int stage) {
     const i32x4 r = make_vsharp(base, (int64_t)rows * k_st * 2);
     const uint32_t st = lds_addr(ks + stage * kStage);
+    constexpr int kRowsPerInst = 64 / kChunks;  // rows covered by one wave instruction
 #pragma unroll
     for (int i = 0; i < kDmaPer; ++i) {
-      const int ch = i * kWaves + wave;
-      dma16(__builtin_amdgcn_readfirstlane(st + ch * kBK * 16), k_dma_off, r, i * kWaves * 16);
+      const int slot0 = (i * kDmaWaves + wave % kDmaWaves) * 64;
+      dma16(st + slot0 * 16, k_dma_off, r, i * kDmaWaves * kRowsPerInst * k_st * 2);
     }
   }
   __device__ __forceinline__ void dma_v(const uint16_t* base, int rows, int stage) {
@@ -239,8 +276,8 @@ struct Attn {
     constexpr int kRowsPerInst = 64 / kChunks;  // rows covered by one wave instruction
 #pragma unroll
     for (int i = 0; i < kDmaPer; ++i) {
-      const int slot0 = (i * kWaves + wave) * 64;
-      dma16(__builtin_amdgcn_readfirstlane(st + slot0 * 16), v_dma_off, r, i * kWaves * kRowsPerInst * v_st * 2);
+      const int slot0 = (i * kDmaWaves + wave % kDmaWaves) * 64;
+      dma16(st + slot0 * 16, v_dma_off, r, i * kDmaWaves * kRowsPerInst * v_st * 2);
     }
   }
   __device__ __forceinline__ int tile_rows(int j) const {
@@ -256,16 +293,19 @@ struct Attn {
   template <bool QK, bool PV>
   __device__ __forceinline__ void mfma_slot(int st_k, int st_v) {
     constexpr int kN = D / 8;  // MFMAs of each kind (QK: D/16 x 2 key blocks; PV: 4 key groups x D/32)
-    constexpr int kAhead = 3;
+    constexpr int kAhead = FASTVR_AHEAD;
     constexpr int kReads = (QK ? 1 : 0) + (PV ? 2 : 0);
     constexpr int kMfma = (QK ? 1 : 0) + (PV ? 1 : 0);
-    const uint16_t* kst = ks + st_k * kStage + k_rd;
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
+    const char* kst = reinterpret_cast<const char*>(ks + st_k * kStage);
     const char* vst = reinterpret_cast<const char*>(vs + st_v * kStage);
 #pragma unroll
     for (int i = 0; i < kN; ++i) {
       if (QK) {
         const int kk = i >> 1, mb = i & 1;
-        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + ((2 * kk) * kBK + mb * 32) * 8);
+        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_rd[kk] + mb * 32 * (D * 2));
         s[mb] = (kk == 0) ? mfma32(a, qf[kk], f32x16{}) : mfma32(a, qf[kk], s[mb]);
       }
       if (PV) {
@@ -285,6 +325,9 @@ struct Attn {
       if (i + kAhead < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kReads, 0);
     }
 #endif
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
   }
 
   // Online softmax of the scores in s[] (MASK: keys at tile positions >= n_valid
@@ -293,7 +336,8 @@ struct Attn {
   template <bool MASK>
   __device__ __forceinline__ void softmax(int n_valid) {
     constexpr float kInf = __builtin_inff();
-    float mx = NEG ? kInf : -kInf;
+    // four independent partial extrema (short dependency chains)
+    float part[4] = {NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf};
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -303,8 +347,11 @@ struct Attn {
           const int key = mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
           x = (key < n_valid) ? x : (NEG ? kInf : -kInf);
         }
-        mx = NEG ? __builtin_fminf(mx, x) : __builtin_fmaxf(mx, x);
+        float& pm = part[v & 3];
+        pm = NEG ? __builtin_fminf(pm, x) : __builtin_fmaxf(pm, x);
       }
+    float mx = NEG ? __builtin_fminf(__builtin_fminf(part[0], part[1]), __builtin_fminf(part[2], part[3]))
+                   : __builtin_fmaxf(__builtin_fmaxf(part[0], part[1]), __builtin_fmaxf(part[2], part[3]));
     float other;
     const float mine = swap_halves(mx, &other);
     mx = NEG ? __builtin_fminf(mine, other) : __builtin_fmaxf(mine, other);
@@ -312,20 +359,28 @@ struct Attn {
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
     m_run = m_new;
     const float nm = -m_new;
-    float psum = 0.f;
+    // in place and in separate passes, so no temporary ties one exp2 to the next
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][v], c, nm));
+        float t = __builtin_fmaf(s[mb][v], c, nm);
         if (MASK) {
           const int key = mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          p = (key < n_valid) ? p : 0.f;
+          t = (key < n_valid) ? t : -kInf;
         }
-        s[mb][v] = p;
-        psum += p;
+        s[mb][v] = t;
       }
-    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(s[mb][v]);
+    float ps[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};  // four independent partial sums
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int v = (mb == 0 ? 4 : 0); v < 16; ++v) ps[v & 3] += s[mb][v];
+    l_run = l_run * alpha + ((ps[0] + ps[1]) + (ps[2] + ps[3]));
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       bf16x8 b;
@@ -387,9 +442,14 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
 
   // prologue: K(0), K(1), V(0) to LDS, Q fragments to registers
   const int64_t k_step = (int64_t)kBK * a.k_st, v_step = (int64_t)kBK * a.v_st;
-  a.dma_k(a.kb + (int64_t)a.lo * a.k_st, a.tile_rows(0), 0);
-  a.dma_k(a.kb + (int64_t)a.lo * a.k_st + k_step, a.tile_rows(1), 1);
-  a.dma_v(a.vb + (int64_t)a.lo * a.v_st, a.tile_rows(0), 0);
+  // K DMA is issued by group B (or everyone), V DMA by group A (or everyone)
+  const bool k_issuer = !FASTVR_DMA_SPLIT || group == 1;
+  const bool v_issuer = !FASTVR_DMA_SPLIT || group == 0;
+  if (k_issuer) {
+    a.dma_k(a.kb + (int64_t)a.lo * a.k_st, a.tile_rows(0), 0);
+    a.dma_k(a.kb + (int64_t)a.lo * a.k_st + k_step, a.tile_rows(1), 1);
+  }
+  if (v_issuer) a.dma_v(a.vb + (int64_t)a.lo * a.v_st, a.tile_rows(0), 0);
   {
     const int rows = (q_end - q0 < kBQ) ? q_end - q0 : kBQ;
     const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (int64_t)b * p.q_sb + (int64_t)q0 * p.q_st + (int64_t)h * D,
@@ -409,12 +469,13 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   // sees the Q loads complete and inserts no further vmcnt waits for them
   __builtin_amdgcn_s_waitcnt(0x0F70);
   barrier();
-  constexpr int kBatch = 2 * A::kDmaPer;  // DMA instructions per wave per batch (one K and one V tile)
+  // DMA instructions a wave issues per iteration (one K and one V tile, or one of them when split)
+  constexpr int kBatch = FASTVR_DMA_SPLIT ? A::kDmaPer : 2 * A::kDmaPer;
 
   // Slot 2j: group A runs MFMA(j) = S(j) and P(j-1).V(j-1); group B the softmax of tile j-1.
   // Slot 2j+1: group A the softmax of tile j; group B MFMA(j).
-  // Before slot 2j the DMA of K(j+2) and V(j+1) is issued (zeros past the end); the
-  // barrier closing slot 2j+1 waits for the batch issued two slots earlier.  Tile j
+  // Slot 2j starts the DMA of K(j+2), slot 2j+1 that of V(j+1) (zeros past the
+  // end); the barrier closing slot 2j+1 waits for the pair issued two slots earlier.  Tile j
   // lives in LDS stage j % 3, so K(j+2) reuses the stage of tile j-1 and V(j+1)
   // the third one.  The first tile, the last tile (the only one that can be
   // ragged) and the drain (j = n) are peeled out of the loop.
@@ -422,12 +483,12 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   const uint16_t* v_next = a.vb + (int64_t)a.lo * a.v_st + v_step;      // V(j+1)
   int st_cur = 0, st_prev = 2, st_next = 1;  // stages of tiles j, j-1 (== j+2) and j+1
   // j = 0
-  a.dma_k(k_next, a.tile_rows(2), st_prev);
-  a.dma_v(v_next, a.tile_rows(1), st_next);
+  if (k_issuer) a.dma_k(k_next, a.tile_rows(2), st_prev);
   k_next += k_step;
-  v_next += v_step;
   if (active && group == 0) a.template mfma_slot<true, false>(st_cur, 0);
   barrier();
+  if (v_issuer) a.dma_v(v_next, a.tile_rows(1), st_next);
+  v_next += v_step;
   if (active) {
     if (group == 0) {
       if (n == 1)
@@ -445,11 +506,9 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
     st_cur = st_next;
     st_next = (st_next == 2) ? 0 : st_next + 1;
     for (int j = 1; j + 1 < n; ++j) {
-      a.dma_k(k_next, a.tile_rows(j + 2), st_prev);
-      a.dma_v(v_next, a.tile_rows(j + 1), st_next);
-      k_next += k_step;
-      v_next += v_step;
       // ---- slot 2j ----
+      if (k_issuer) a.dma_k(k_next, a.tile_rows(j + 2), st_prev);
+      k_next += k_step;
       if (active) {
         if (group == 0)
           a.template mfma_slot<true, true>(st_cur, st_prev);
@@ -458,6 +517,8 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       }
       barrier();
       // ---- slot 2j+1 ----
+      if (v_issuer) a.dma_v(v_next, a.tile_rows(j + 1), st_next);
+      v_next += v_step;
       if (active) {
         if (group == 0)
           a.template softmax<false>(kBK);
