@@ -62,13 +62,13 @@ constexpr int kBufFlags = 0x00020000;     // raw buffer, 32-bit data format (gfx
 #define FASTVR_SCHED 1
 #endif
 #ifndef FASTVR_PRIO
-#define FASTVR_PRIO 0
+#define FASTVR_PRIO 1
 #endif
 #ifndef FASTVR_AHEAD
 #define FASTVR_AHEAD 3
 #endif
 #ifndef FASTVR_DMA_SPLIT
-#define FASTVR_DMA_SPLIT 0
+#define FASTVR_DMA_SPLIT 1
 #endif
 static_assert(kBQ == kFwdRowsPerItem, "tile height mismatch");
 
