@@ -17,10 +17,15 @@
 //
 // Matrix-core / vector-ALU ping-pong: waves 0-3 (group A) and 4-7 (group B)
 // share the four SIMDs one-to-one.  Time is cut into slots separated by
-// workgroup barriers; in every slot one group runs only MFMAs (scores of tile
-// j and P.V of tile j-1) while the other runs only the online softmax of its
-// last scores, and the roles swap each slot.  Each SIMD therefore always has a
-// matrix-core wave and a vector-ALU wave side by side.
+// workgroup barriers, and the two groups swap roles every slot:
+//  * matrix-core slot: the 16 QK MFMAs of tile j, then the 16 P.V MFMAs of tile
+//    j-1 with the row statistics of the new scores (running maximum, rescale
+//    factor, s * c - m) issued between them, so that this wave's vector-ALU
+//    work hides under its own matrix-core time;
+//  * vector-ALU slot: exp2, row sums, bf16 rounding of P and the rescale of O,
+//    plus the DMA of the next K or V tile.
+// Each SIMD therefore always has a matrix-core wave and a vector-ALU wave side
+// by side.
 //
 // Memory: all K and V tiles (64 keys) travel by DMA straight from HBM into LDS
 // (buffer_load ... lds, per-tile buffer descriptors: rows outside the visible
@@ -46,10 +51,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = kFwdThreads / 64;  // 8
@@ -58,6 +61,12 @@ constexpr int kBK = 64;                   // keys per KV tile
 constexpr int kStages = 3;                // LDS buffers per operand
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kBufFlags = 0x00020000;     // raw buffer, 32-bit data format (gfx9 family)
+// Tuning switches (compile time):
+//  FASTVR_SCHED      order MFMAs, LDS reads and vector-ALU work with scheduling groups
+//  FASTVR_PRIO       raise the wave priority during matrix-core slots
+//  FASTVR_AHEAD      MFMA operand reads kept in flight ahead of their MFMA
+//  FASTVR_VALU_PER   row-statistics instructions placed after each P.V MFMA
+//  FASTVR_DMA_SPLIT  1: the four vector-ALU waves of a slot issue its DMA; 0: all eight
 #ifndef FASTVR_SCHED
 #define FASTVR_SCHED 1
 #endif
@@ -65,7 +74,10 @@ constexpr int kBufFlags = 0x00020000;     // raw buffer, 32-bit data format (gfx
 #define FASTVR_PRIO 1
 #endif
 #ifndef FASTVR_AHEAD
-#define FASTVR_AHEAD 3
+#define FASTVR_AHEAD 6
+#endif
+#ifndef FASTVR_VALU_PER
+#define FASTVR_VALU_PER 4
 #endif
 #ifndef FASTVR_DMA_SPLIT
 #define FASTVR_DMA_SPLIT 1
@@ -127,7 +139,12 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i32x4 rs
   rsrc.w = __builtin_amdgcn_readfirstlane(rsrc.w);
   soff = __builtin_amdgcn_readfirstlane(soff);
   lds_addr = __builtin_amdgcn_readfirstlane(lds_addr);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+  // s_nop 4: the scalar operands may have just been written by v_readfirstlane
+  // (a vector-ALU write of an SGPR needs 5 wait states before a buffer
+  // instruction reads it); s_nop 0: one wait state between the M0 write and
+  // the LDS-DMA that reads M0.  Hazards inside inline assembly are not
+  // covered by the compiler.
+  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
                : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
                : "memory", "m0");
@@ -169,6 +186,7 @@ __device__ __forceinline__ void wait_vmcnt<4>() { asm volatile("s_waitcnt vmcnt(
 // instruction-group ordering hints for the scheduler (sched_group_barrier masks)
 #define SCHED_MFMA 0x008
 #define SCHED_DS_READ 0x100
+#define SCHED_VALU 0x002
 
 // blockIdx -> (local query chunk, batch*head, tile).  Workgroups are handed to
 // the 8 XCDs round-robin; within each full round of 256 workgroups the
@@ -228,6 +246,7 @@ struct Attn {
   f32x16 s[2];
   u32x4 pf[4];
   float m_run, l_run;
+  float alpha;  // rescale factor of the tile whose statistics were taken last
 
   // XOR applied to the 16-byte chunk index of K row r: 16 consecutive rows read
   // the same logical chunk from 16 distinct bank groups
@@ -260,83 +279,62 @@ struct Attn {
 
   // DMA of one K (or V) tile: `base` points at the tile's first key row, `rows`
   // valid rows (0 past the end of the interval: the stage is filled with zeros).
-  __device__ __forceinline__ void dma_k(const uint16_t* base, int rows, int stage) {
-    const i32x4 r = make_vsharp(base, (int64_t)rows * k_st * 2);
-    const uint32_t st = lds_addr(ks + stage * kStage);
+  // A tile is kDmaPer instructions per issuing wave; a DmaJob holds what they share.
+  struct DmaJob {
+    i32x4 rsrc;
+    uint32_t lds;
+  };
+  template <bool IS_K>
+  __device__ __forceinline__ DmaJob dma_job(const uint16_t* base, int rows, int stage) const {
+    const int st = IS_K ? k_st : v_st;
+    return DmaJob{make_vsharp(base, (int64_t)rows * st * 2), lds_addr((IS_K ? ks : vs) + stage * kStage)};
+  }
+  template <bool IS_K>
+  __device__ __forceinline__ void dma_inst(const DmaJob& jb, int i) const {
     constexpr int kRowsPerInst = 64 / kChunks;  // rows covered by one wave instruction
+    const int slot0 = (i * kDmaWaves + wave % kDmaWaves) * 64;
+    const int st = IS_K ? k_st : v_st;
+    dma16(jb.lds + slot0 * 16, IS_K ? k_dma_off : v_dma_off, jb.rsrc, i * kDmaWaves * kRowsPerInst * st * 2);
+  }
+  __device__ __forceinline__ void dma_k(const uint16_t* base, int rows, int stage) {
+    const DmaJob jb = dma_job<true>(base, rows, stage);
 #pragma unroll
-    for (int i = 0; i < kDmaPer; ++i) {
-      const int slot0 = (i * kDmaWaves + wave % kDmaWaves) * 64;
-      dma16(st + slot0 * 16, k_dma_off, r, i * kDmaWaves * kRowsPerInst * k_st * 2);
-    }
+    for (int i = 0; i < kDmaPer; ++i) dma_inst<true>(jb, i);
   }
   __device__ __forceinline__ void dma_v(const uint16_t* base, int rows, int stage) {
-    const i32x4 r = make_vsharp(base, (int64_t)rows * v_st * 2);
-    const uint32_t st = lds_addr(vs + stage * kStage);
-    constexpr int kRowsPerInst = 64 / kChunks;  // rows covered by one wave instruction
+    const DmaJob jb = dma_job<false>(base, rows, stage);
 #pragma unroll
-    for (int i = 0; i < kDmaPer; ++i) {
-      const int slot0 = (i * kDmaWaves + wave % kDmaWaves) * 64;
-      dma16(st + slot0 * 16, v_dma_off, r, i * kDmaWaves * kRowsPerInst * v_st * 2);
-    }
+    for (int i = 0; i < kDmaPer; ++i) dma_inst<false>(jb, i);
   }
   __device__ __forceinline__ int tile_rows(int j) const {
     const int r = hi - (lo + j * kBK);
     return r <= 0 ? 0 : (r < kBK ? r : kBK);
   }
 
-  // One matrix-core slot: S^T(tile in st_k) = K Q^T (QK) and/or
-  // O^T += V^T P^T (tile in st_v, PV).  The QK and PV MFMAs are interleaved
-  // (six independent accumulators) and the LDS operand reads run kAhead MFMA
-  // pairs ahead.  K fragments: one 16-byte read; V^T fragments: two transpose
-  // reads of 4 keys each.
-  template <bool QK, bool PV>
-  __device__ __forceinline__ void mfma_slot(int st_k, int st_v) {
-    constexpr int kN = D / 8;  // MFMAs of each kind (QK: D/16 x 2 key blocks; PV: 4 key groups x D/32)
-    constexpr int kAhead = FASTVR_AHEAD;
-    constexpr int kReads = (QK ? 1 : 0) + (PV ? 2 : 0);
-    constexpr int kMfma = (QK ? 1 : 0) + (PV ? 1 : 0);
-#if FASTVR_PRIO
-    __builtin_amdgcn_s_setprio(1);
-#endif
-    const char* kst = reinterpret_cast<const char*>(ks + st_k * kStage);
-    const char* vst = reinterpret_cast<const char*>(vs + st_v * kStage);
-#pragma unroll
-    for (int i = 0; i < kN; ++i) {
-      if (QK) {
-        const int kk = i >> 1, mb = i & 1;
-        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_rd[kk] + mb * 32 * (D * 2));
-        s[mb] = (kk == 0) ? mfma32(a, qf[kk], f32x16{}) : mfma32(a, qf[kk], s[mb]);
-      }
-      if (PV) {
-        const int g = i / (D / 32), dm = i % (D / 32);
-        const char* base = vst + v_rd[dm] + g * 16 * (D * 2);
-        const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
-        const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * (D * 2)));
-        const i16x8 a8 = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[dm] = mfma32(__builtin_bit_cast(u32x4, a8), pf[g], o[dm]);
-      }
-    }
-#if FASTVR_SCHED
-    __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kAhead * kReads, 0);
-#pragma unroll
-    for (int i = 0; i < kN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, kMfma, 0);
-      if (i + kAhead < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kReads, 0);
-    }
-#endif
-#if FASTVR_PRIO
-    __builtin_amdgcn_s_setprio(0);
-#endif
+  __device__ __forceinline__ u32x4 read_k(const char* kst, int i) const {
+    const int kk = i >> 1, mb = i & 1;
+    return *reinterpret_cast<const u32x4*>(kst + k_rd[kk] + mb * 32 * (D * 2));
   }
 
-  // Online softmax of the scores in s[] (MASK: keys at tile positions >= n_valid
-  // lie outside the visible interval): new running maximum, rescale of O and l,
-  // P = exp2(s*c - m) rounded to bf16 fragments, running sum from the fp32 P.
+  __device__ __forceinline__ i16x8 read_vt(const char* vst, int i) const {
+    const int g = i / (D / 32), dm = i % (D / 32);
+    const char* base = vst + v_rd[dm] + g * 16 * (D * 2);
+    const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
+    const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * (D * 2)));
+    return __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+  }
+
+  // Row statistics of the fresh scores s[] (tile positions >= n_valid lie
+  // outside the visible interval): running maximum m (log2 domain), alpha =
+  // 2^(m_old - m), and s <- s * c - m in place, ready for exp2.
   template <bool MASK>
-  __device__ __forceinline__ void softmax(int n_valid) {
+  __device__ __forceinline__ void row_stats(int n_valid) {
     constexpr float kInf = __builtin_inff();
-    // four independent partial extrema (short dependency chains)
+    // keys of this lane: mb * 32 + 8 * (v >> 2) + (v & 3) + 4 * hh; the limit is
+    // made opaque so that the compares are not shared with another call site
+    // and kept alive across the main loop
+    int lim = n_valid - 4 * hh;
+    if (MASK) asm volatile("" : "+v"(lim));
     float part[4] = {NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf};
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
@@ -344,8 +342,8 @@ struct Attn {
       for (int v = 0; v < 16; ++v) {
         float x = s[mb][v];
         if (MASK) {
-          const int key = mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          x = (key < n_valid) ? x : (NEG ? kInf : -kInf);
+          const int key = mb * 32 + 8 * (v >> 2) + (v & 3);
+          x = (key < lim) ? x : (NEG ? kInf : -kInf);
         }
         float& pm = part[v & 3];
         pm = NEG ? __builtin_fminf(pm, x) : __builtin_fmaxf(pm, x);
@@ -356,26 +354,30 @@ struct Attn {
     const float mine = swap_halves(mx, &other);
     mx = NEG ? __builtin_fminf(mine, other) : __builtin_fmaxf(mine, other);
     const float m_new = __builtin_fmaxf(m_run, mx * c);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
+    alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
     m_run = m_new;
     const float nm = -m_new;
-    // in place and in separate passes, so no temporary ties one exp2 to the next
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float t = __builtin_fmaf(s[mb][v], c, nm);
         if (MASK) {
-          const int key = mb * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          t = (key < n_valid) ? t : -kInf;
+          const int key = mb * 32 + 8 * (v >> 2) + (v & 3);
+          t = (key < lim) ? t : -kInf;
         }
         s[mb][v] = t;
       }
+  }
+
+  // The rest of the online softmax once row_stats has run: P = exp2(t) rounded
+  // to bf16 fragments, l = l * alpha + rowsum(P), O *= alpha.
+  __device__ __forceinline__ void softmax_rest() {
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(s[mb][v]);
-    float ps[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};  // four independent partial sums
+    float ps[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -394,11 +396,86 @@ struct Attn {
     }
   }
 
+  // One matrix-core slot: S^T(tile in st_k) = K Q^T (QK), then
+  // O^T += V^T P^T (tile in st_v, PV) with, when STATS, the row statistics of
+  // the new scores interleaved (FASTVR_VALU_PER vector-ALU instructions after
+  // each P.V MFMA).  The two phases are separate scheduling regions; K and V^T
+  // operand reads run kAhead MFMAs ahead, and the first V^T reads are issued
+  // during the last QK MFMAs.  K fragments: one 16-byte read; V^T fragments:
+  // two transpose reads of 4 keys each.
+  template <bool QK, bool PV, bool STATS>
+  __device__ __forceinline__ void mfma_slot(int st_k, int st_v) {
+    constexpr int kN = D / 8;  // MFMAs of each kind (QK: D/16 x 2 key blocks; PV: 4 key groups x D/32)
+    constexpr int kAhead = FASTVR_AHEAD < kN ? FASTVR_AHEAD : kN;
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
+    const char* kst = reinterpret_cast<const char*>(ks + st_k * kStage);
+    const char* vst = reinterpret_cast<const char*>(vs + st_v * kStage);
+    i16x8 vt[kN];
+    u32x4 kf[kN];
+    if (QK) {
+#pragma unroll
+      for (int i = 0; i < kAhead; ++i) kf[i] = read_k(kst, i);
+#pragma unroll
+      for (int i = 0; i < kN; ++i) {
+        if (i + kAhead < kN)
+          kf[i + kAhead] = read_k(kst, i + kAhead);
+        else if (PV)
+          vt[i + kAhead - kN] = read_vt(vst, i + kAhead - kN);
+        const int kk = i >> 1, mb = i & 1;
+        s[mb] = (kk == 0) ? mfma32(kf[i], qf[kk], f32x16{}) : mfma32(kf[i], qf[kk], s[mb]);
+      }
+#if FASTVR_SCHED
+      __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kAhead, 0);
+#pragma unroll
+      for (int i = 0; i < kN; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+        if (i + kAhead < kN)
+          __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+        else if (PV)
+          __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2, 0);
+      }
+#endif
+      __builtin_amdgcn_sched_barrier(0);
+    } else if (PV) {
+#pragma unroll
+      for (int i = 0; i < kAhead; ++i) vt[i] = read_vt(vst, i);
+    }
+    if (PV) {
+#pragma unroll
+      for (int i = 0; i < kN; ++i) {
+        if (i + kAhead < kN) vt[i + kAhead] = read_vt(vst, i + kAhead);
+        const int g = i / (D / 32), dm = i % (D / 32);
+        o[dm] = mfma32(__builtin_bit_cast(u32x4, vt[i]), pf[g], o[dm]);
+      }
+    }
+    if (STATS) row_stats<false>(kBK);
+#if FASTVR_SCHED
+    if (PV) {
+      if (!QK) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2 * kAhead, 0);
+#pragma unroll
+      for (int i = 0; i < kN; ++i) {
+        if (i + kAhead < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+        if (STATS) __builtin_amdgcn_sched_group_barrier(SCHED_VALU, FASTVR_VALU_PER, 0);
+      }
+    }
+#endif
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
+  }
+
+  // Online softmax of the last tile (the only one that can be ragged): its
+  // statistics, masked when the tile holds fewer than kBK visible keys, are
+  // taken here rather than in the matrix-core slot.
   __device__ __forceinline__ void softmax_last(int last_valid) {
     if (last_valid < kBK)
-      softmax<true>(last_valid);
+      row_stats<true>(last_valid);
     else
-      softmax<false>(kBK);
+      row_stats<false>(kBK);
+    softmax_rest();
   }
 };
 
@@ -442,7 +519,8 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
 
   // prologue: K(0), K(1), V(0) to LDS, Q fragments to registers
   const int64_t k_step = (int64_t)kBK * a.k_st, v_step = (int64_t)kBK * a.v_st;
-  // K DMA is issued by group B (or everyone), V DMA by group A (or everyone)
+  // K DMA is issued by group B (or everyone), V DMA by group A (or everyone):
+  // the group in its vector-ALU slot
   const bool k_issuer = !FASTVR_DMA_SPLIT || group == 1;
   const bool v_issuer = !FASTVR_DMA_SPLIT || group == 0;
   if (k_issuer) {
@@ -469,23 +547,32 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   // sees the Q loads complete and inserts no further vmcnt waits for them
   __builtin_amdgcn_s_waitcnt(0x0F70);
   barrier();
+
   // DMA instructions a wave issues per iteration (one K and one V tile, or one of them when split)
   constexpr int kBatch = FASTVR_DMA_SPLIT ? A::kDmaPer : 2 * A::kDmaPer;
 
-  // Slot 2j: group A runs MFMA(j) = S(j) and P(j-1).V(j-1); group B the softmax of tile j-1.
-  // Slot 2j+1: group A the softmax of tile j; group B MFMA(j).
+  // Slot 2j: group A runs the matrix-core slot of tile j (S(j), P(j-1).V(j-1),
+  // statistics of S(j)); group B the vector-ALU slot of tile j-1.
+  // Slot 2j+1: group A the vector-ALU slot of tile j; group B the matrix-core
+  // slot of tile j.
   // Slot 2j starts the DMA of K(j+2), slot 2j+1 that of V(j+1) (zeros past the
-  // end); the barrier closing slot 2j+1 waits for the pair issued two slots earlier.  Tile j
-  // lives in LDS stage j % 3, so K(j+2) reuses the stage of tile j-1 and V(j+1)
-  // the third one.  The first tile, the last tile (the only one that can be
-  // ragged) and the drain (j = n) are peeled out of the loop.
+  // end); the barrier closing slot 2j+1 waits for the pair issued two slots
+  // earlier.  Tile j lives in LDS stage j % 3, so K(j+2) reuses the stage of
+  // tile j-1 and V(j+1) the third one.  The first tile, the last tile (the
+  // only one that can be ragged; its statistics are taken in the vector-ALU
+  // slot) and the drain (j = n) are peeled out of the loop.
   const uint16_t* k_next = a.kb + (int64_t)a.lo * a.k_st + 2 * k_step;  // K(j+2)
   const uint16_t* v_next = a.vb + (int64_t)a.lo * a.v_st + v_step;      // V(j+1)
   int st_cur = 0, st_prev = 2, st_next = 1;  // stages of tiles j, j-1 (== j+2) and j+1
   // j = 0
   if (k_issuer) a.dma_k(k_next, a.tile_rows(2), st_prev);
   k_next += k_step;
-  if (active && group == 0) a.template mfma_slot<true, false>(st_cur, 0);
+  if (active && group == 0) {
+    if (n == 1)
+      a.template mfma_slot<true, false, false>(st_cur, 0);
+    else
+      a.template mfma_slot<true, false, true>(st_cur, 0);
+  }
   barrier();
   if (v_issuer) a.dma_v(v_next, a.tile_rows(1), st_next);
   v_next += v_step;
@@ -494,9 +581,12 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       if (n == 1)
         a.softmax_last(last_valid);
       else
-        a.template softmax<false>(kBK);
+        a.softmax_rest();
     } else {
-      a.template mfma_slot<true, false>(st_cur, 0);
+      if (n == 1)
+        a.template mfma_slot<true, false, false>(st_cur, 0);
+      else
+        a.template mfma_slot<true, false, true>(st_cur, 0);
     }
   }
   wait_vmcnt<kBatch>();
@@ -511,9 +601,9 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       k_next += k_step;
       if (active) {
         if (group == 0)
-          a.template mfma_slot<true, true>(st_cur, st_prev);
+          a.template mfma_slot<true, true, true>(st_cur, st_prev);
         else
-          a.template softmax<false>(kBK);
+          a.softmax_rest();
       }
       barrier();
       // ---- slot 2j+1 ----
@@ -521,9 +611,9 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       v_next += v_step;
       if (active) {
         if (group == 0)
-          a.template softmax<false>(kBK);
+          a.softmax_rest();
         else
-          a.template mfma_slot<true, true>(st_cur, st_prev);
+          a.template mfma_slot<true, true, true>(st_cur, st_prev);
       }
       wait_vmcnt<kBatch>();
       barrier();
@@ -534,16 +624,16 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
     // j = n - 1: last tile (no further DMA)
     if (active) {
       if (group == 0)
-        a.template mfma_slot<true, true>(st_cur, st_prev);
+        a.template mfma_slot<true, true, false>(st_cur, st_prev);
       else
-        a.template softmax<false>(kBK);
+        a.softmax_rest();
     }
     barrier();
     if (active) {
       if (group == 0)
         a.softmax_last(last_valid);
       else
-        a.template mfma_slot<true, true>(st_cur, st_prev);
+        a.template mfma_slot<true, true, false>(st_cur, st_prev);
     }
   }
   wait_vmcnt<0>();
@@ -551,12 +641,12 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   // j = n: drain, P(n-1).V(n-1)
   if (active) {
     if (group == 0)
-      a.template mfma_slot<false, true>(0, st_cur);
+      a.template mfma_slot<false, true, false>(0, st_cur);
     else
       a.softmax_last(last_valid);
   }
   barrier();
-  if (active && group == 1) a.template mfma_slot<false, true>(0, st_cur);
+  if (active && group == 1) a.template mfma_slot<false, true, false>(0, st_cur);
   if (!active) return;
 
   // epilogue: the two halves of the wave hold partial sums over disjoint keys
