@@ -10,6 +10,8 @@ from .chunk_attention import (  # noqa: F401
     key_chunks,
     kv_cache_append,
     query_chunks,
+    ring_slot,
+    ring_step,
     softmax_weights,
     visibility_mask,
 )

@@ -225,3 +225,59 @@ def kv_cache_append(k_cache, v_cache, k_new, v_new, cache_len: int):
     kc[:, cache_len:cache_len + n_new] = k_new
     vc[:, cache_len:cache_len + n_new] = v_new
     return kc, vc
+
+
+# ---------------------------------------------------------------------------
+# Bounded ring KV cache (streaming with an O(k) cache, Sec. 3.1, last paragraph)
+# ---------------------------------------------------------------------------
+
+def ring_slot(chunk_index: int, window_chunks: int) -> int:
+    """Slot of chunk ``chunk_index`` in a ring of ``window_chunks + 1`` chunk slots."""
+    return chunk_index % (window_chunks + 1)
+
+
+def ring_step(k_ring, v_ring, q_new, k_new, v_new, chunk_len: int, chunk_index: int,
+              window_chunks: int, scale=None):
+    """One streaming step with a ring cache of W + 1 chunk slots.
+
+    The ring ([B, (W + 1) * chunk_len, H, d]) holds chunk c in token rows
+    ``[slot * chunk_len, slot * chunk_len + chunk_len)`` with
+    ``slot = c mod (W + 1)``.  The step writes the new chunk c (``n_new <=
+    chunk_len`` tokens of queries, keys and values) into its slot and returns
+    the attention of its queries over the keys of chunks ``max(0, c - W) .. c``,
+    read from the ring in chunk order, with the chunk-causal mask of Eq. 1
+    (queries of chunk c see all of those keys; inside chunk c attention is
+    bidirectional).  Earlier chunks are taken as full (``chunk_len`` tokens).
+
+    Returns ``(o, lse, k_ring_after, v_ring_after)``.  The memory of the ring
+    stays ``W + 1`` chunks however long the stream is, which is the paper's
+    O(k) cache for a fixed chunk size."""
+    W = int(window_chunks)
+    if W < 0:
+        raise ValueError("a ring cache needs a bounded window (window_chunks >= 0)")
+    L = int(chunk_len)
+    c = int(chunk_index)
+    kr = np.array(k_ring, copy=True)
+    vr = np.array(v_ring, copy=True)
+    n_new = np.shape(k_new)[1]
+    if not 1 <= n_new <= L:
+        raise ValueError("the new chunk must hold 1 .. chunk_len tokens")
+    if kr.shape[1] != (W + 1) * L:
+        raise ValueError("the ring must hold (window_chunks + 1) * chunk_len tokens")
+    s = ring_slot(c, W)
+    kr[:, s * L:s * L + n_new] = k_new
+    vr[:, s * L:s * L + n_new] = v_new
+    # gather the visible chunks in chunk order: c - n_prev .. c
+    n_prev = min(c, W)
+    ks, vs = [], []
+    for cc in range(c - n_prev, c + 1):
+        sc = ring_slot(cc, W)
+        rows = L if cc < c else n_new
+        ks.append(kr[:, sc * L:sc * L + rows])
+        vs.append(vr[:, sc * L:sc * L + rows])
+    k_seq = np.concatenate(ks, axis=1)
+    v_seq = np.concatenate(vs, axis=1)
+    # in the gathered sequence the new chunk has chunk index n_prev
+    o, lse = attention(q_new, k_seq, v_seq, chunk_len=L, q_chunk_offset=n_prev,
+                       window_chunks=W, scale=scale)
+    return o, lse, kr, vr

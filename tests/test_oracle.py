@@ -391,3 +391,85 @@ def test_pins_catch_transposed_scores(monkeypatch):
     o1, _ = bad(q, k, v, chunk_len=4, window_chunks=1, scale=0.5)
     o2, _ = oracle.brute_force(q, k, v, 1, 4, 0, 1, scale=0.5)
     assert np.abs(o1 - o2).max() > 1e-6
+
+
+# ---------------------------------------------------------------------------
+# bounded ring KV cache (W + 1 chunk slots; streaming with an O(k) cache)
+# ---------------------------------------------------------------------------
+
+def _stream_through_ring(q, k, v, L, W, scale, step=None):
+    """Feed a whole sequence chunk by chunk through oracle.ring_step; return the
+    concatenated outputs and the ring after every step."""
+    step = step or oracle.ring_step
+    B, N, H, d = q.shape
+    kr = np.full((B, (W + 1) * L, H, d), np.nan)  # never-written slots must not be read
+    vr = np.full_like(kr, np.nan)
+    outs, lses, rings = [], [], []
+    for c in range(-(-N // L)):
+        s = slice(c * L, min((c + 1) * L, N))
+        o, lse, kr, vr = step(kr, vr, q[:, s], k[:, s], v[:, s], L, c, W, scale)
+        outs.append(o)
+        lses.append(lse)
+        rings.append((kr.copy(), vr.copy()))
+    return np.concatenate(outs, axis=1), np.concatenate(lses, axis=2), rings
+
+
+@pytest.mark.parametrize("W,L,N", [(0, 5, 23), (1, 5, 23), (1, 8, 32), (1, 1, 6), (2, 7, 40), (3, 4, 9)])
+def test_ring_streaming_equals_parallel(W, L, N):
+    """Streaming chunk by chunk through a ring of W + 1 slots gives every chunk
+    the rows of the parallel chunk-causal call with window W (the streaming and
+    parallel forms of Sec. 3.1 agree), including a ragged last chunk."""
+    q, k, v = _rand(2, N, N, 2, 8, seed=60 + W + L)
+    o_ring, lse_ring, _ = _stream_through_ring(q, k, v, L, W, scale=0.3)
+    o_par, lse_par = oracle.attention(q, k, v, chunk_len=L, window_chunks=W, scale=0.3)
+    np.testing.assert_allclose(o_ring, o_par, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse_ring, lse_par, rtol=0, atol=1e-12)
+
+
+def test_ring_streaming_matches_frame_level_eq1():
+    """Eq. 1 itself (W = 1, frame-level mask, brute force) equals the ring stream."""
+    hw, kf, T = 3, 2, 7  # 3 tokens per latent frame, 2 frames per chunk, 7 frames
+    N, L = hw * T, hw * kf
+    q, k, v = _rand(1, N, N, 1, 4, seed=71)
+    o_bf, lse_bf = oracle.brute_force(q, k, v, hw, kf, 0, 1, scale=0.4)
+    o_ring, lse_ring, _ = _stream_through_ring(q, k, v, L, 1, scale=0.4)
+    np.testing.assert_allclose(o_ring, o_bf, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse_ring, lse_bf, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W", [0, 1, 2])
+def test_ring_holds_the_last_w_plus_one_chunks(W):
+    """After step c the ring holds chunks c - W .. c in slots (chunk mod (W + 1)),
+    and its size never grows with the stream (the O(k) cache)."""
+    L, N = 4, 30
+    q, k, v = _rand(1, N, N, 1, 8, seed=80 + W)
+    _, _, rings = _stream_through_ring(q, k, v, L, W, scale=0.5)
+    for c, (kr, vr) in enumerate(rings):
+        assert kr.shape[1] == (W + 1) * L
+        for cc in range(max(0, c - W), c + 1):
+            s = cc % (W + 1)
+            n = min(L, N - cc * L)
+            np.testing.assert_array_equal(kr[:, s * L:s * L + n], k[:, cc * L:cc * L + n])
+            np.testing.assert_array_equal(vr[:, s * L:s * L + n], v[:, cc * L:cc * L + n])
+
+
+def test_ring_step_rejects_unbounded_window_and_bad_sizes():
+    kr = np.zeros((1, 8, 1, 4))
+    x = np.zeros((1, 4, 1, 4))
+    with pytest.raises(ValueError):
+        oracle.ring_step(kr, kr, x, x, x, 4, 0, -1)
+    with pytest.raises(ValueError):
+        oracle.ring_step(kr, kr, np.zeros((1, 5, 1, 4)), np.zeros((1, 5, 1, 4)), np.zeros((1, 5, 1, 4)), 4, 0, 1)
+    with pytest.raises(ValueError):
+        oracle.ring_step(np.zeros((1, 12, 1, 4)), np.zeros((1, 12, 1, 4)), x, x, x, 4, 0, 1)
+
+
+def test_ring_pins_catch_a_wrong_slot(monkeypatch):
+    """A ring that puts chunk c in slot c mod W (one slot too few) fails the
+    streaming == parallel pin."""
+    monkeypatch.setattr(oc, "ring_slot", lambda c, W: c % max(W, 1))
+    q, k, v = _rand(1, 20, 20, 1, 8, seed=90)
+    with pytest.raises((AssertionError, ValueError)):
+        o_ring, _, _ = _stream_through_ring(q, k, v, 5, 1, scale=0.3)
+        o_par, _ = oracle.attention(q, k, v, chunk_len=5, window_chunks=1, scale=0.3)
+        np.testing.assert_allclose(o_ring, o_par, rtol=0, atol=1e-12)
