@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 1
+#define FASTVR_ABI_VERSION 2
 
 typedef enum {
   FASTVR_OK = 0,
@@ -109,6 +109,43 @@ fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k
                                      const void* v_new, int64_t B, int64_t H, int64_t d,
                                      int64_t capacity, int64_t cache_len, int64_t n_new,
                                      void* stream);
+
+/*
+ * Streaming step with a bounded ring KV cache (Sec. 3.1, last paragraph:
+ * streaming inference with KV caching, whose cache size stays O(k) for a
+ * fixed chunk size k, independent of the video length).  The ring holds
+ * W + 1 chunk slots, W = window_chunks (Eq. 1 is W = 1):
+ *   k_ring, v_ring  bf16 [B, (W + 1) * chunk_len, H, d] contiguous
+ * Chunk c of the stream occupies token rows s * chunk_len .. s * chunk_len +
+ * chunk_len - 1 of slot s = c mod (W + 1).  For the new chunk c = chunk_index,
+ * given
+ *   q_new, k_new, v_new  bf16 [B, n_new, H, d] contiguous   its tokens,
+ * one kernel
+ *   1. computes the attention of q_new over the keys and values of chunks
+ *      max(0, c - W) .. c in chunk order: chunk c from k_new / v_new, the earlier
+ *      ones from their ring slots (they must be full chunks written by the
+ *      previous steps of the same stream);
+ *   2. writes k_new / v_new into slot c mod (W + 1) (the append, fused into the
+ *      same launch; the slot held chunk c - W - 1, which chunk c does not see).
+ * Outputs o fp32 [B, n_new, H, d] and lse fp32 [B, H, n_new] (or NULL) equal,
+ * for the rows of chunk c, those of fastvr_chunk_attn_fwd over the whole
+ * sequence with the same window_chunks.
+ *
+ * Preconditions (else FASTVR_ERR_INVALID_ARGUMENT unless noted):
+ *  - all pointers except lse non-NULL and 16-byte aligned, lse NULL or 4-byte
+ *    aligned; the ring, o and lse overlap no other argument;
+ *  - B, H >= 0; 1 <= n_new <= chunk_len; chunk_index >= 0; 0 <= W;
+ *  - W <= 7, d in {64, 128} and chunk_len a multiple of 4 (d = 128) or 8
+ *    (d = 64), so that no DMA row group of the kernel straddles two chunks
+ *    (else FASTVR_ERR_UNSUPPORTED);
+ *  - scale finite; no element count overflows int64.
+ * B or H equal to 0: FASTVR_OK, nothing enqueued.
+ */
+fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, const void* v_new,
+                                          void* k_ring, void* v_ring, float* o, float* lse, int64_t B,
+                                          int64_t H, int64_t n_new, int64_t d, int64_t chunk_len,
+                                          int64_t chunk_index, int64_t window_chunks, float scale,
+                                          void* stream);
 
 /* Static string naming a status code ("FASTVR_OK", ...); never NULL. */
 const char* fastvr_status_string(fastvr_status s);

@@ -95,7 +95,15 @@ struct Params {
   int32_t nq, nkv, chunk_len, q_chunk_offset, window;  // window -1 = unbounded
   int32_t B, H, n_local_chunks, tiles_full, tiles_last, n_items;
   float c;  // scale * log2(e)
+  // Bounded ring cache (ring step only): key rows are virtual rows over the
+  // visible chunks in chunk order; chunk s < n_seg - 1 is read from ring slot
+  // (ring_first + s) mod ring_slots, the last (new) one from k / v above.
+  uint16_t* rk;
+  uint16_t* rv;
+  int64_t ring_sb;  // batch stride of the ring (elements); token stride = k_st
+  int32_t ring_slots, ring_first, n_seg, new_slot, ring_chunk;  // ring_chunk: tokens per slot
 };
+constexpr int kMaxRingSlots = 8;
 
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
@@ -219,7 +227,7 @@ __device__ __forceinline__ void decode_item(const Params& p, int i, int& cl, int
   }
 }
 
-template <int D, bool NEG>
+template <int D, bool NEG, bool RING>
 struct Attn {
   static constexpr int kChunks = D / 8;                        // 16-byte chunks per key row
   static constexpr int kStage = kBK * D;                       // bf16 elements per stage (K or V)
@@ -239,6 +247,10 @@ struct Attn {
   const uint16_t* vb;
   int k_st, v_st;
   uint32_t k_dma_off, v_dma_off;  // per-lane byte offsets of this wave's DMA rows
+  // ring step: ring bases of this (batch, head), chunk length, slots
+  const uint16_t* rkb;
+  const uint16_t* rvb;
+  int ring_L, ring_slots, ring_first, n_seg, n_last;
   int k_rd[D / 16];                // byte offsets of this lane's K operand reads (row n, chunk 2kk + hh)
   int v_rd[D / 32];                // byte offsets of this lane's V^T transpose reads
   u32x4 qf[D / 16];
@@ -306,6 +318,59 @@ struct Attn {
 #pragma unroll
     for (int i = 0; i < kDmaPer; ++i) dma_inst<false>(jb, i);
   }
+  // Ring step: DMA instruction i of the tile starting at virtual key row t0.
+  // Its kRowsPerInst rows lie in one chunk (the host requires chunk_len to be a
+  // multiple of kRowsPerInst), so one buffer descriptor covers them: the ring
+  // slot of that chunk, or the new chunk's k / v; rows past the chunk's end
+  // read as zero.
+  template <bool IS_K>
+  __device__ __forceinline__ void dma_inst_ring(int t0, int stage, int i) const {
+    constexpr int kRowsPerInst = 64 / kChunks;
+    const int oi = (i * kDmaWaves + wave % kDmaWaves) * kRowsPerInst;
+    const int r0 = t0 + oi;
+    int seg = 0;
+#pragma unroll
+    for (int m = 1; m < kMaxRingSlots; ++m)
+      if (m < n_seg && r0 >= m * ring_L) seg = m;
+    const int in_seg = r0 - seg * ring_L;
+    const int st = IS_K ? k_st : v_st;
+    const uint16_t* base;
+    int len;
+    if (seg == n_seg - 1) {
+      base = IS_K ? kb : vb;
+      len = n_last;
+    } else {
+      int slot = ring_first + seg;
+      if (slot >= ring_slots) slot -= ring_slots;
+      base = (IS_K ? rkb : rvb) + (int64_t)slot * ring_L * st;
+      len = ring_L;
+    }
+    const int rows = len - in_seg;
+    const i32x4 r = make_vsharp(base + (int64_t)in_seg * st, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    // per-lane offset within the instruction's rows: drop this wave's row offset
+    const uint32_t off = (IS_K ? k_dma_off : v_dma_off) - (uint32_t)((wave % kDmaWaves) * kRowsPerInst * st * 2);
+    const uint32_t la = lds_addr((IS_K ? ks : vs) + stage * kStage) + (uint32_t)((i * kDmaWaves + wave % kDmaWaves) * 64 * 16);
+    dma16(la, off, r, 0);
+  }
+
+  // DMA of K (or V) tile j (64 keys from lo + 64 j) into LDS stage `stage`
+  __device__ __forceinline__ void load_k(int j, int stage) {
+    if (RING) {
+#pragma unroll
+      for (int i = 0; i < kDmaPer; ++i) dma_inst_ring<true>(lo + j * kBK, stage, i);
+    } else {
+      dma_k(kb + (int64_t)(lo + j * kBK) * k_st, tile_rows(j), stage);
+    }
+  }
+  __device__ __forceinline__ void load_v(int j, int stage) {
+    if (RING) {
+#pragma unroll
+      for (int i = 0; i < kDmaPer; ++i) dma_inst_ring<false>(lo + j * kBK, stage, i);
+    } else {
+      dma_v(vb + (int64_t)(lo + j * kBK) * v_st, tile_rows(j), stage);
+    }
+  }
+
   __device__ __forceinline__ int tile_rows(int j) const {
     const int r = hi - (lo + j * kBK);
     return r <= 0 ? 0 : (r < kBK ? r : kBK);
@@ -479,9 +544,9 @@ struct Attn {
   }
 };
 
-template <int D, bool NEG>
+template <int D, bool NEG, bool RING>
 __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Params p) {
-  using A = Attn<D, NEG>;
+  using A = Attn<D, NEG, RING>;
   __shared__ __attribute__((aligned(16))) uint16_t smem[A::kLdsElems];
   A a;
   a.ks = smem;
@@ -510,6 +575,15 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   a.vb = p.v + (int64_t)b * p.v_sb + (int64_t)h * D;
   a.k_st = p.k_st;
   a.v_st = p.v_st;
+  if (RING) {
+    a.rkb = p.rk + (int64_t)b * p.ring_sb + (int64_t)h * D;
+    a.rvb = p.rv + (int64_t)b * p.ring_sb + (int64_t)h * D;
+    a.ring_L = p.ring_chunk;
+    a.ring_slots = p.ring_slots;
+    a.ring_first = p.ring_first;
+    a.n_seg = p.n_seg;
+    a.n_last = p.nq;  // the new chunk: as many keys as queries
+  }
   a.init_offsets();
 
   const int row = q0 + a.wave * 32 + a.n;
@@ -518,16 +592,15 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   const int last_valid = a.hi - (a.lo + (n - 1) * kBK);  // keys in the last tile
 
   // prologue: K(0), K(1), V(0) to LDS, Q fragments to registers
-  const int64_t k_step = (int64_t)kBK * a.k_st, v_step = (int64_t)kBK * a.v_st;
   // K DMA is issued by group B (or everyone), V DMA by group A (or everyone):
   // the group in its vector-ALU slot
   const bool k_issuer = !FASTVR_DMA_SPLIT || group == 1;
   const bool v_issuer = !FASTVR_DMA_SPLIT || group == 0;
   if (k_issuer) {
-    a.dma_k(a.kb + (int64_t)a.lo * a.k_st, a.tile_rows(0), 0);
-    a.dma_k(a.kb + (int64_t)a.lo * a.k_st + k_step, a.tile_rows(1), 1);
+    a.load_k(0, 0);
+    a.load_k(1, 1);
   }
-  if (v_issuer) a.dma_v(a.vb + (int64_t)a.lo * a.v_st, a.tile_rows(0), 0);
+  if (v_issuer) a.load_v(0, 0);
   {
     const int rows = (q_end - q0 < kBQ) ? q_end - q0 : kBQ;
     const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + (int64_t)b * p.q_sb + (int64_t)q0 * p.q_st + (int64_t)h * D,
@@ -561,12 +634,9 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   // tile j-1 and V(j+1) the third one.  The first tile, the last tile (the
   // only one that can be ragged; its statistics are taken in the vector-ALU
   // slot) and the drain (j = n) are peeled out of the loop.
-  const uint16_t* k_next = a.kb + (int64_t)a.lo * a.k_st + 2 * k_step;  // K(j+2)
-  const uint16_t* v_next = a.vb + (int64_t)a.lo * a.v_st + v_step;      // V(j+1)
   int st_cur = 0, st_prev = 2, st_next = 1;  // stages of tiles j, j-1 (== j+2) and j+1
   // j = 0
-  if (k_issuer) a.dma_k(k_next, a.tile_rows(2), st_prev);
-  k_next += k_step;
+  if (k_issuer) a.load_k(2, st_prev);
   if (active && group == 0) {
     if (n == 1)
       a.template mfma_slot<true, false, false>(st_cur, 0);
@@ -574,8 +644,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       a.template mfma_slot<true, false, true>(st_cur, 0);
   }
   barrier();
-  if (v_issuer) a.dma_v(v_next, a.tile_rows(1), st_next);
-  v_next += v_step;
+  if (v_issuer) a.load_v(1, st_next);
   if (active) {
     if (group == 0) {
       if (n == 1)
@@ -597,8 +666,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
     st_next = (st_next == 2) ? 0 : st_next + 1;
     for (int j = 1; j + 1 < n; ++j) {
       // ---- slot 2j ----
-      if (k_issuer) a.dma_k(k_next, a.tile_rows(j + 2), st_prev);
-      k_next += k_step;
+      if (k_issuer) a.load_k(j + 2, st_prev);
       if (active) {
         if (group == 0)
           a.template mfma_slot<true, true, true>(st_cur, st_prev);
@@ -607,8 +675,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
       }
       barrier();
       // ---- slot 2j+1 ----
-      if (v_issuer) a.dma_v(v_next, a.tile_rows(j + 1), st_next);
-      v_next += v_step;
+      if (v_issuer) a.load_v(j + 1, st_next);
       if (active) {
         if (group == 0)
           a.softmax_rest();
@@ -647,6 +714,30 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   }
   barrier();
   if (active && group == 1) a.template mfma_slot<false, true, false>(0, st_cur);
+  if (RING) {
+    // fused append: this workgroup's share of the new chunk's K and V goes to
+    // ring slot new_slot (a slot no query of this call reads)
+    const int64_t hd8 = (int64_t)p.H * D / 8;        // 16-byte units per token
+    const int64_t per_b = (int64_t)p.nq * hd8;        // units per batch row
+    const int64_t total = per_b * p.B;
+    const int64_t share = (total + p.n_items - 1) / p.n_items;
+    const int64_t u0 = (int64_t)blockIdx.x * share;
+    const int64_t u1 = (u0 + share < total) ? u0 + share : total;
+    for (int bb = 0; bb < p.B; ++bb) {
+      const int64_t lo_u = (u0 > bb * per_b) ? u0 : bb * per_b;
+      const int64_t hi_u = (u1 < (bb + 1) * per_b) ? u1 : (bb + 1) * per_b;
+      if (lo_u >= hi_u) continue;
+      const u32x4* ksrc = reinterpret_cast<const u32x4*>(p.k + (int64_t)bb * p.k_sb);
+      const u32x4* vsrc = reinterpret_cast<const u32x4*>(p.v + (int64_t)bb * p.v_sb);
+      const int64_t dst = (int64_t)bb * p.ring_sb + (int64_t)p.new_slot * p.ring_chunk * p.k_st;
+      u32x4* kd = reinterpret_cast<u32x4*>(p.rk + dst);
+      u32x4* vd = reinterpret_cast<u32x4*>(p.rv + dst);
+      for (int64_t u = lo_u - bb * per_b + tid; u < hi_u - bb * per_b; u += kFwdThreads) {
+        kd[u] = ksrc[u];
+        vd[u] = vsrc[u];
+      }
+    }
+  }
   if (!active) return;
 
   // epilogue: the two halves of the wave hold partial sums over disjoint keys
@@ -673,8 +764,13 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
 }
 
 template <int D, bool NEG>
-hipError_t launch_t(const Params& p, int64_t n_items, hipStream_t stream) {
-  hipLaunchKernelGGL((chunk_attn_fwd_kernel<D, NEG>), dim3((unsigned)n_items), dim3(kFwdThreads), 0, stream, p);
+hipError_t launch_t(const Params& p, bool ring, int64_t n_items, hipStream_t stream) {
+  if (ring)
+    hipLaunchKernelGGL((chunk_attn_fwd_kernel<D, NEG, true>), dim3((unsigned)n_items), dim3(kFwdThreads), 0, stream,
+                       p);
+  else
+    hipLaunchKernelGGL((chunk_attn_fwd_kernel<D, NEG, false>), dim3((unsigned)n_items), dim3(kFwdThreads), 0, stream,
+                       p);
   return hipGetLastError();
 }
 
@@ -720,9 +816,19 @@ hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   p.tiles_last = (int32_t)g.tiles_last;
   p.n_items = (int32_t)g.n_items;
   p.c = a.scale * 1.44269504088896340736f;
+  const bool ring = a.k_ring != nullptr;
+  p.rk = static_cast<uint16_t*>(a.k_ring);
+  p.rv = static_cast<uint16_t*>(a.v_ring);
+  p.ring_sb = a.ring_sb;
+  p.ring_slots = (int32_t)a.ring_slots;
+  p.ring_first = (int32_t)a.ring_first;
+  p.n_seg = (int32_t)a.n_seg;
+  p.new_slot = (int32_t)a.new_slot;
+  p.ring_chunk = (int32_t)a.chunk_len;
   const bool neg = p.c < 0.f;
-  if (a.d == 128) return neg ? launch_t<128, true>(p, g.n_items, stream) : launch_t<128, false>(p, g.n_items, stream);
-  return neg ? launch_t<64, true>(p, g.n_items, stream) : launch_t<64, false>(p, g.n_items, stream);
+  if (a.d == 128)
+    return neg ? launch_t<128, true>(p, ring, g.n_items, stream) : launch_t<128, false>(p, ring, g.n_items, stream);
+  return neg ? launch_t<64, true>(p, ring, g.n_items, stream) : launch_t<64, false>(p, ring, g.n_items, stream);
 }
 
 }  // namespace fastvr

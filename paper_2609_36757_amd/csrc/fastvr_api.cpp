@@ -88,10 +88,17 @@ fastvr_status check_view(const View& w, int64_t B, int64_t hd, int64_t* bytes) {
   return FASTVR_OK;
 }
 
+struct Ring {
+  void* k = nullptr;
+  void* v = nullptr;
+  int64_t sb = 0, slots = 0, first = 0, n_seg = 0, new_slot = 0, bytes = 0;
+};
+
 fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k, int64_t k_sb, int64_t k_st,
                        const void* v, int64_t v_sb, int64_t v_st, float* o, int64_t o_sb, int64_t o_st, float* lse,
                        int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
-                       int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+                       int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream,
+                       const Ring& ring = Ring()) {
   if (B < 0 || H < 0 || Nq < 0 || Nkv < 0)
     return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld H=%lld Nq=%lld Nkv=%lld)", (long long)B,
                 (long long)H, (long long)Nq, (long long)Nkv);
@@ -118,8 +125,10 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
   int64_t qb, kb, vb, ob;
   fastvr_status s;
   if ((s = check_view({"q", q, q_sb, q_st, Nq, 2}, B, hd, &qb)) != FASTVR_OK) return s;
-  if ((s = check_view({"k", k, k_sb, k_st, Nkv, 2}, B, hd, &kb)) != FASTVR_OK) return s;
-  if ((s = check_view({"v", v, v_sb, v_st, Nkv, 2}, B, hd, &vb)) != FASTVR_OK) return s;
+  // k / v rows in memory: all Nkv key rows, or in a ring step only the new chunk
+  const int64_t kv_rows = ring.k != nullptr ? Nq : Nkv;
+  if ((s = check_view({"k", k, k_sb, k_st, kv_rows, 2}, B, hd, &kb)) != FASTVR_OK) return s;
+  if ((s = check_view({"v", v, v_sb, v_st, kv_rows, 2}, B, hd, &vb)) != FASTVR_OK) return s;
   if ((s = check_view({"o", o, o_sb, o_st, Nq, 4}, B, hd, &ob)) != FASTVR_OK) return s;
   if (q_st >= fastvr::kMaxTokenStride || k_st >= fastvr::kMaxTokenStride || v_st >= fastvr::kMaxTokenStride ||
       o_st >= fastvr::kMaxTokenStride)
@@ -135,6 +144,16 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
   if (lse != nullptr && (overlap(lse, lb, q, qb) || overlap(lse, lb, k, kb) || overlap(lse, lb, v, vb) ||
                          overlap(lse, lb, o, ob)))
     return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse overlaps q, k, v or o");
+  if (ring.k != nullptr) {
+    const void* others[5] = {q, k, v, o, lse};
+    const int64_t sizes[5] = {qb, kb, vb, ob, lb};
+    for (int i = 0; i < 5; ++i)
+      if (others[i] != nullptr && (overlap(ring.k, ring.bytes, others[i], sizes[i]) ||
+                                   overlap(ring.v, ring.bytes, others[i], sizes[i])))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "the ring overlaps q_new, k_new, v_new, o or lse");
+    if (overlap(ring.k, ring.bytes, ring.v, ring.bytes))
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "k_ring and v_ring overlap");
+  }
 
   const fastvr::FwdGrid g = fastvr::fwd_grid(B, H, Nq, chunk_len);
   if (g.n_items > fastvr::kMaxFwdItems)
@@ -152,6 +171,13 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
   a.q_chunk_offset = q_chunk_offset;
   a.window_chunks = window_chunks;
   a.scale = scale;
+  a.k_ring = ring.k;
+  a.v_ring = ring.v;
+  a.ring_sb = ring.sb;
+  a.ring_slots = ring.slots;
+  a.ring_first = ring.first;
+  a.n_seg = ring.n_seg;
+  a.new_slot = ring.new_slot;
   const hipError_t e = fastvr::launch_chunk_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "chunk_attn_fwd launch failed: %s", hipGetErrorString(e));
   return ok();
@@ -179,6 +205,55 @@ fastvr_status fastvr_chunk_attn_fwd_ex(const void* q, int64_t q_sb, int64_t q_st
                                        int64_t window_chunks, float scale, void* stream) {
   return fwd_impl(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, B, H, Nq, Nkv, d, chunk_len,
                   q_chunk_offset, window_chunks, scale, stream);
+}
+
+fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, const void* v_new, void* k_ring,
+                                          void* v_ring, float* o, float* lse, int64_t B, int64_t H, int64_t n_new,
+                                          int64_t d, int64_t chunk_len, int64_t chunk_index, int64_t window_chunks,
+                                          float scale, void* stream) {
+  if (B < 0 || H < 0 || n_new < 0 || chunk_len < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld H=%lld n_new=%lld chunk_len=%lld)",
+                (long long)B, (long long)H, (long long)n_new, (long long)chunk_len);
+  if (chunk_index < 0) return fail(FASTVR_ERR_INVALID_ARGUMENT, "chunk_index %lld < 0", (long long)chunk_index);
+  if (window_chunks < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "a ring cache needs window_chunks >= 0 (got %lld)",
+                (long long)window_chunks);
+  if (window_chunks > fastvr::kMaxRingWindow)
+    return fail(FASTVR_ERR_UNSUPPORTED, "window_chunks %lld > %lld", (long long)window_chunks,
+                (long long)fastvr::kMaxRingWindow);
+  if (d != 64 && d != 128) return fail(FASTVR_ERR_UNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)d);
+  if (n_new < 1 || n_new > chunk_len)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "n_new = %lld must be in 1 .. chunk_len = %lld", (long long)n_new,
+                (long long)chunk_len);
+  const int64_t rows_per_dma = d == 128 ? 4 : 8;
+  if (chunk_len % rows_per_dma != 0)
+    return fail(FASTVR_ERR_UNSUPPORTED, "chunk_len %lld is not a multiple of %lld (head_dim %lld)",
+                (long long)chunk_len, (long long)rows_per_dma, (long long)d);
+  if (k_ring == nullptr || v_ring == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "k_ring or v_ring is NULL");
+  if (!aligned(k_ring, 16) || !aligned(v_ring, 16))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "k_ring or v_ring is not 16-byte aligned");
+  Ring r;
+  r.slots = window_chunks + 1;
+  int64_t hd, ring_rows, n_prev, nkv;
+  if (!mul_ok(H, d, &hd) || !mul_ok(r.slots, chunk_len, &ring_rows) || !mul_ok(ring_rows, hd, &r.sb) ||
+      !mul_ok(B, r.sb, &r.bytes) || !mul_ok(r.bytes, 2, &r.bytes))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  n_prev = chunk_index < window_chunks ? chunk_index : window_chunks;  // earlier visible chunks
+  if (!mul_ok(n_prev, chunk_len, &nkv) || !add_ok(nkv, n_new, &nkv))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  if (ring_rows > INT32_MAX) return fail(FASTVR_ERR_UNSUPPORTED, "ring rows must be below 2^31");
+  r.k = k_ring;
+  r.v = v_ring;
+  r.n_seg = n_prev + 1;
+  r.new_slot = chunk_index % r.slots;
+  r.first = (chunk_index - n_prev) % r.slots;
+  int64_t sn = 0;
+  if (!mul_ok(n_new, hd, &sn)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  // queries: the new chunk, which is chunk n_prev of the visible sequence; keys:
+  // the visible chunks, virtual rows 0 .. nkv - 1 (the kernel reads the earlier
+  // ones from the ring and the new one from k_new / v_new)
+  return fwd_impl(q_new, sn, hd, k_new, sn, hd, v_new, sn, hd, o, sn, hd, lse, B, H, n_new, nkv, d, chunk_len,
+                  n_prev, window_chunks, scale, stream, r);
 }
 
 fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new, int64_t B,

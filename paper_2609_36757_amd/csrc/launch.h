@@ -20,7 +20,17 @@ struct FwdArgs {
   int64_t B, H, nq, nkv, d;
   int64_t chunk_len, q_chunk_offset, window_chunks;
   float scale;
+  // Ring step (k_ring != nullptr): k / v are the new chunk, the earlier visible
+  // chunks come from the ring; the kernel also writes k / v into new_slot.
+  void* k_ring = nullptr;
+  void* v_ring = nullptr;
+  int64_t ring_sb = 0;      // batch stride of the ring (elements)
+  int64_t ring_slots = 0;   // window_chunks + 1
+  int64_t ring_first = 0;   // slot of the oldest visible chunk
+  int64_t n_seg = 0;        // visible chunks (the new one included)
+  int64_t new_slot = 0;     // slot of the new chunk
 };
+constexpr int64_t kMaxRingWindow = 7;  // window_chunks of a ring step
 
 // Work decomposition of one forward call (host side, also used for checks).
 struct FwdGrid {

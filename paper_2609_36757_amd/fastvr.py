@@ -19,7 +19,7 @@ ERR_CAPACITY = 3
 ERR_HIP = 4
 
 EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
-            "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
+            "fastvr_chunk_attn_ring_step", "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
 
 _i64 = ctypes.c_int64
 _vp = ctypes.c_void_p
@@ -49,6 +49,9 @@ def load() -> ctypes.CDLL:
                                              ctypes.c_float, _vp]
     lib.fastvr_kv_cache_append.restype = ctypes.c_int
     lib.fastvr_kv_cache_append.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _vp]
+    lib.fastvr_chunk_attn_ring_step.restype = ctypes.c_int
+    lib.fastvr_chunk_attn_ring_step.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
+                                                _i64, _i64, ctypes.c_float, _vp]
     lib.fastvr_status_string.restype = ctypes.c_char_p
     lib.fastvr_status_string.argtypes = [ctypes.c_int]
     lib.fastvr_last_error.restype = ctypes.c_char_p
@@ -91,6 +94,12 @@ def fwd_ex_raw(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, 
 def append_raw(k_cache, v_cache, k_new, v_new, B, H, d, capacity, cache_len, n_new, stream=0) -> int:
     return load().fastvr_kv_cache_append(k_cache, v_cache, k_new, v_new, B, H, d, capacity, cache_len,
                                          n_new, stream)
+
+
+def ring_step_raw(q_new, k_new, v_new, k_ring, v_ring, o, lse, B, H, n_new, d, chunk_len, chunk_index,
+                  window_chunks, scale, stream=0) -> int:
+    return load().fastvr_chunk_attn_ring_step(q_new, k_new, v_new, k_ring, v_ring, o, lse, B, H, n_new, d,
+                                              chunk_len, chunk_index, window_chunks, scale, stream)
 
 
 # ---------------------------------------------------------------------------
@@ -166,3 +175,40 @@ def kv_cache_append(k_cache, v_cache, k_new, v_new, cache_len: int, stream=None)
     _check(append_raw(k_cache.data_ptr(), v_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), B, H, d, cap,
                       cache_len, n_new, _stream_handle(stream)))
     return cache_len + n_new
+
+
+def chunk_attn_ring_step(q_new, k_new, v_new, k_ring, v_ring, *, chunk_len: int, chunk_index: int,
+                         window_chunks: int = 1, scale: float | None = None, out=None, lse=None,
+                         return_lse: bool = True, stream=None):
+    """One streaming step with a bounded ring KV cache of window_chunks + 1 chunk slots.
+
+    q_new/k_new/v_new [B, n_new, H, d] bf16 hold chunk ``chunk_index`` of the
+    stream; k_ring/v_ring [B, (window_chunks + 1) * chunk_len, H, d] bf16 hold
+    the earlier chunks (chunk c in slot c mod (window_chunks + 1)).  The library
+    writes the new chunk into its slot and returns (o fp32 [B, n_new, H, d],
+    lse fp32 [B, H, n_new] or None) over chunks chunk_index - window_chunks ..
+    chunk_index.  All tensors contiguous."""
+    import torch
+    for name, t in (("q_new", q_new), ("k_new", k_new), ("v_new", v_new), ("k_ring", k_ring), ("v_ring", v_ring)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor")
+    B, n_new, H, d = q_new.shape
+    if k_new.shape != q_new.shape or v_new.shape != q_new.shape:
+        raise ValueError("q_new, k_new and v_new must have the same shape")
+    if k_ring.shape != (B, (window_chunks + 1) * chunk_len, H, d) or v_ring.shape != k_ring.shape:
+        raise ValueError("k_ring/v_ring must be [B, (window_chunks + 1) * chunk_len, H, d]")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    if out is None:
+        out = torch.empty((B, n_new, H, d), dtype=torch.float32, device=q_new.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != (B, n_new, H, d) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 [B, n_new, H, d] tensor")
+    if return_lse and lse is None:
+        lse = torch.empty((B, H, n_new), dtype=torch.float32, device=q_new.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, n_new)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [B, H, n_new] tensor")
+    _check(ring_step_raw(q_new.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_ring.data_ptr(), v_ring.data_ptr(),
+                         out.data_ptr(), lse.data_ptr() if lse is not None else None, B, H, n_new, d, chunk_len,
+                         chunk_index, window_chunks, scale, _stream_handle(stream)))
+    return out, lse

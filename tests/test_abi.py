@@ -14,7 +14,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 # Distinct fake addresses, 1 TiB apart, for calls that must fail validation:
 # every case below is rejected on the host before the HIP runtime is touched.
-Q, K, V, O, LSE = ((i + 1) << 40 for i in range(5))
+Q, K, V, O, LSE, RK, RV = ((i + 1) << 40 for i in range(7))
 BIG = 1 << 62
 
 
@@ -40,7 +40,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 1
+    assert lib.fastvr_abi_version() == 2
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -152,6 +152,47 @@ def test_append_rejects(lib, kw, status, needle):
 @pytest.mark.parametrize("kw", [dict(n_new=0), dict(B=0), dict(H=0)])
 def test_append_empty_is_ok(lib, kw):
     assert _app(**kw) == fastvr.OK
+
+
+RING_GOOD = dict(q=Q, k=K, v=V, rk=RK, rv=RV, o=O, lse=LSE, B=1, H=2, n_new=64, d=128, chunk_len=64,
+                 chunk_index=3, window_chunks=1, scale=0.125)
+
+
+def _ring(**kw):
+    a = dict(RING_GOOD)
+    a.update(kw)
+    return fastvr.ring_step_raw(a["q"], a["k"], a["v"], a["rk"], a["rv"], a["o"], a["lse"], a["B"], a["H"],
+                                a["n_new"], a["d"], a["chunk_len"], a["chunk_index"], a["window_chunks"],
+                                a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(window_chunks=-1), fastvr.ERR_INVALID_ARGUMENT, "window_chunks >= 0"),
+    (dict(window_chunks=8), fastvr.ERR_UNSUPPORTED, "window_chunks 8 > 7"),
+    (dict(n_new=0), fastvr.ERR_INVALID_ARGUMENT, "n_new"),
+    (dict(n_new=65), fastvr.ERR_INVALID_ARGUMENT, "n_new"),
+    (dict(chunk_len=66, n_new=60), fastvr.ERR_UNSUPPORTED, "multiple of 4"),
+    (dict(chunk_len=68, n_new=60, d=64), fastvr.ERR_UNSUPPORTED, "multiple of 8"),
+    (dict(chunk_index=-1), fastvr.ERR_INVALID_ARGUMENT, "chunk_index"),
+    (dict(d=96), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(rk=None), fastvr.ERR_INVALID_ARGUMENT, "k_ring or v_ring is NULL"),
+    (dict(rv=RV + 8), fastvr.ERR_INVALID_ARGUMENT, "16-byte aligned"),
+    (dict(q=None), fastvr.ERR_INVALID_ARGUMENT, "q is NULL"),
+    (dict(scale=float("nan")), fastvr.ERR_INVALID_ARGUMENT, "scale"),
+    (dict(rk=O + 256), fastvr.ERR_INVALID_ARGUMENT, "ring overlaps"),
+    (dict(rk=K + 512), fastvr.ERR_INVALID_ARGUMENT, "ring overlaps"),
+    (dict(rv=RK + 4096), fastvr.ERR_INVALID_ARGUMENT, "k_ring and v_ring overlap"),
+    (dict(B=-1), fastvr.ERR_INVALID_ARGUMENT, "negative size"),
+    (dict(chunk_len=1 << 40, n_new=64), fastvr.ERR_UNSUPPORTED, "2^31"),
+])
+def test_ring_step_rejects(lib, kw, status, needle):
+    assert _ring(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(H=0)])
+def test_ring_step_empty_is_ok(lib, kw):
+    assert _ring(**kw) == fastvr.OK
 
 
 def test_error_is_thread_local(lib):
