@@ -9,7 +9,11 @@ One step = the whole hot path on one batch of synthetic input resident in HBM:
 value = effective (unmasked) TFLOP/s of the whole step: 4 * d * visible pairs
 * B * H for both attention calls, divided by the step time.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+After the timed steps (and outside them) it reports ms/call and TFLOP/s of
+the 480p-shaped and wide sliding-window calls and of the W = 1 ring-cache
+streaming step (``other_workloads``), then the fp64 oracle baseline.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra]
 """
 from __future__ import annotations
 
@@ -78,6 +82,59 @@ def cpu_baseline(w, q, k, v, budget_rows: int, seed: int = 0):
                       f"{dt:.1f} s wall, fp64 NumPy/BLAS, host os.cpu_count()={os.cpu_count()}"}
 
 
+def _time_ms(torch, cur, fn, reps: int, warm: int = 2) -> float:
+    """Average ms of fn() over reps calls, HIP events on the launch stream."""
+    for _ in range(warm):
+        fn()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record(cur)
+    for _ in range(reps):
+        fn()
+    e.record(cur)
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / reps
+
+
+def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
+    """ms/call and effective TFLOP/s of the other synthetic workloads: the
+    480p-shaped and the wide sliding-window parallel calls, and the paper's
+    W = 1 streaming step with the bounded ring cache at the 1080p chunk shape."""
+    from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence
+    res = {}
+    for name, reps in (("480p", 20), ("wide_sw", 3)):
+        w = WORKLOADS[name]
+        q, k, v = (t.to(dev) for t in make_sequence(w))
+        o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
+        lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
+        ms = _time_ms(torch, cur, lambda: fastvr.chunk_attn(q, k, v, chunk_len=w.chunk_len,
+                                                            window_chunks=w.window_chunks, scale=w.scale,
+                                                            out=o, lse=lse), reps)
+        f = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
+        res[name] = {"ms": round(ms, 4), "ms_per_chunk": round(ms / w.n_chunks, 4),
+                     "tflops": round(f / (ms * 1e-3) / 1e12, 2), "frac_of_bf16_peak": round(f / (ms * 1e-3) / 1e12
+                                                                                          / PEAK_BF16_TFLOPS, 4)}
+        del q, k, v, o, lse
+    # W = 1 ring step: chunk 3 of the 1080p sequence, chunk 2 already in the ring
+    w = w1080
+    L, c = w.chunk_len, 3
+    ring_k = torch.empty((w.B, 2 * L, w.H, w.d), dtype=torch.bfloat16, device=dev)
+    ring_v = torch.empty_like(ring_k)
+    s_prev = (c - 1) % 2
+    ring_k[:, s_prev * L:(s_prev + 1) * L].copy_(kd[:, (c - 1) * L:c * L])
+    ring_v[:, s_prev * L:(s_prev + 1) * L].copy_(vd[:, (c - 1) * L:c * L])
+    qn, kn, vn = (t[:, c * L:(c + 1) * L].contiguous() for t in (qd, kd, vd))
+    o = torch.empty((w.B, L, w.H, w.d), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.H, L), dtype=torch.float32, device=dev)
+    ms = _time_ms(torch, cur, lambda: fastvr.chunk_attn_ring_step(qn, kn, vn, ring_k, ring_v, chunk_len=L,
+                                                                  chunk_index=c, window_chunks=1, scale=w.scale,
+                                                                  out=o, lse=lse), 20)
+    f = metrics.effective_flops(w.B, w.H, w.d, L, 2 * L, L, 1, 1)
+    res["ring_step_w1_1080p"] = {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2),
+                                 "note": "chunk 3 vs chunks 2-3, append of chunk 3 fused into the launch"}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +143,7 @@ def main():
     ap.add_argument("--workload", default="1080p", choices=["1080p", "480p", "wide_sw", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2560)
+    ap.add_argument("--no-extra", action="store_true", help="skip the 480p / wide_sw / ring-step timings")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build measures the single-GPU kernel "
@@ -205,6 +263,10 @@ def main():
                      "traffic": traffic},
         "wall_s_timed": round(wall, 3),
     }
+    if not args.no_extra:
+        print("[bench] other workloads (not part of the step)", flush=True)
+        del o, lse
+        out["other_workloads"] = other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w)
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (fp64 oracle on a row sample)", flush=True)
         out["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_rows)

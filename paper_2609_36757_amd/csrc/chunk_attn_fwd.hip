@@ -318,54 +318,101 @@ struct Attn {
 #pragma unroll
     for (int i = 0; i < kDmaPer; ++i) dma_inst<false>(jb, i);
   }
-  // Ring step: DMA instruction i of the tile starting at virtual key row t0.
-  // Its kRowsPerInst rows lie in one chunk (the host requires chunk_len to be a
-  // multiple of kRowsPerInst), so one buffer descriptor covers them: the ring
-  // slot of that chunk, or the new chunk's k / v; rows past the chunk's end
-  // read as zero.
+  // Ring step.  Virtual key rows run over the visible chunks in chunk order;
+  // chunk seg < n_seg - 1 lives in ring slot (ring_first + seg) mod ring_slots,
+  // the last one is the new chunk in k / v.
+  struct RingSeg {
+    const uint16_t* base;  // row 0 of the chunk
+    int start;             // virtual row of its first key
+    int len;               // keys it holds
+  };
   template <bool IS_K>
-  __device__ __forceinline__ void dma_inst_ring(int t0, int stage, int i) const {
-    constexpr int kRowsPerInst = 64 / kChunks;
-    const int oi = (i * kDmaWaves + wave % kDmaWaves) * kRowsPerInst;
-    const int r0 = t0 + oi;
-    int seg = 0;
-#pragma unroll
-    for (int m = 1; m < kMaxRingSlots; ++m)
-      if (m < n_seg && r0 >= m * ring_L) seg = m;
-    const int in_seg = r0 - seg * ring_L;
-    const int st = IS_K ? k_st : v_st;
-    const uint16_t* base;
-    int len;
-    if (seg == n_seg - 1) {
-      base = IS_K ? kb : vb;
-      len = n_last;
-    } else {
-      int slot = ring_first + seg;
-      if (slot >= ring_slots) slot -= ring_slots;
-      base = (IS_K ? rkb : rvb) + (int64_t)slot * ring_L * st;
-      len = ring_L;
+  __device__ __forceinline__ RingSeg ring_seg(int seg) const {
+    if (seg >= n_seg - 1) return RingSeg{IS_K ? kb : vb, (n_seg - 1) * ring_L, n_last};
+    int slot = ring_first + seg;
+    if (slot >= ring_slots) slot -= ring_slots;
+    return RingSeg{(IS_K ? rkb : rvb) + (int64_t)slot * ring_L * (IS_K ? k_st : v_st), seg * ring_L, ring_L};
+  }
+  __device__ __forceinline__ int ring_seg_of(int r) const {
+    // chunks are consecutive runs of ring_L virtual rows (scalar loop, n_seg <= 8)
+    int seg = 0, bound = ring_L;
+    while (seg + 1 < n_seg && r >= bound) {
+      ++seg;
+      bound += ring_L;
     }
-    const int rows = len - in_seg;
-    const i32x4 r = make_vsharp(base + (int64_t)in_seg * st, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    return seg;
+  }
+
+  // DMA instruction i of the tile starting at virtual row t0, whose rows all
+  // lie in chunk sg (the host requires chunk_len to be a multiple of the
+  // instruction's kRowsPerInst rows): one buffer descriptor over the rest of
+  // that chunk, so rows past its end read as zero.
+  template <bool IS_K>
+  __device__ __forceinline__ void dma_inst_ring(const RingSeg& sg, int r0, int stage, int i) const {
+    constexpr int kRowsPerInst = 64 / kChunks;
+    const int st = IS_K ? k_st : v_st;
+    const int in_seg = r0 - sg.start;
+    // only this instruction's rows matter: clamp to [0, kRowsPerInst] so the
+    // byte count stays a small 32-bit value
+    int rows = sg.len - in_seg;
+    rows = rows < 0 ? 0 : (rows > kRowsPerInst ? kRowsPerInst : rows);
+    const uint64_t a = (uint64_t)(sg.base + (int64_t)in_seg * st);
+    const i32x4 r = {(int)(uint32_t)a, (int)((a >> 32) & 0xffff), rows * st * 2, kBufFlags};
     // per-lane offset within the instruction's rows: drop this wave's row offset
     const uint32_t off = (IS_K ? k_dma_off : v_dma_off) - (uint32_t)((wave % kDmaWaves) * kRowsPerInst * st * 2);
     const uint32_t la = lds_addr((IS_K ? ks : vs) + stage * kStage) + (uint32_t)((i * kDmaWaves + wave % kDmaWaves) * 64 * 16);
     dma16(la, off, r, 0);
   }
 
+  // One K or V tile of a ring step.  With chunks of at least one tile the tile
+  // touches at most two chunks, looked up once per tile; shorter chunks take
+  // the lookup per instruction.
+  template <bool IS_K>
+  __device__ __forceinline__ void load_ring(int j, int stage) {
+    constexpr int kRowsPerInst = 64 / kChunks;
+    const int t0 = __builtin_amdgcn_readfirstlane(lo + j * kBK);
+    // wave-uniform offset of this wave's rows in the tile (scalar register)
+    const int w0 = __builtin_amdgcn_readfirstlane((wave % kDmaWaves) * kRowsPerInst);
+    if (ring_L >= kBK) {
+      const int seg0 = ring_seg_of(t0);
+      const RingSeg s0 = ring_seg<IS_K>(seg0);
+      if (seg0 + 1 >= n_seg || t0 + kBK <= (seg0 + 1) * ring_L) {
+        // the whole tile lies in one chunk (all but one tile per chunk
+        // boundary): the plain tile DMA from that chunk
+        const int in_seg = t0 - s0.start;
+        const int rows = s0.len - in_seg;
+        if (IS_K)
+          dma_k(s0.base + (int64_t)in_seg * k_st, rows < 0 ? 0 : (rows > kBK ? kBK : rows), stage);
+        else
+          dma_v(s0.base + (int64_t)in_seg * v_st, rows < 0 ? 0 : (rows > kBK ? kBK : rows), stage);
+        return;
+      }
+      const RingSeg s1 = ring_seg<IS_K>(seg0 + 1);
+#pragma unroll
+      for (int i = 0; i < kDmaPer; ++i) {
+        const int r0 = t0 + i * kDmaWaves * kRowsPerInst + w0;
+        dma_inst_ring<IS_K>(r0 >= s1.start ? s1 : s0, r0, stage, i);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kDmaPer; ++i) {
+        const int r0 = t0 + i * kDmaWaves * kRowsPerInst + w0;
+        dma_inst_ring<IS_K>(ring_seg<IS_K>(ring_seg_of(r0)), r0, stage, i);
+      }
+    }
+  }
+
   // DMA of K (or V) tile j (64 keys from lo + 64 j) into LDS stage `stage`
   __device__ __forceinline__ void load_k(int j, int stage) {
     if (RING) {
-#pragma unroll
-      for (int i = 0; i < kDmaPer; ++i) dma_inst_ring<true>(lo + j * kBK, stage, i);
+      load_ring<true>(j, stage);
     } else {
       dma_k(kb + (int64_t)(lo + j * kBK) * k_st, tile_rows(j), stage);
     }
   }
   __device__ __forceinline__ void load_v(int j, int stage) {
     if (RING) {
-#pragma unroll
-      for (int i = 0; i < kDmaPer; ++i) dma_inst_ring<false>(lo + j * kBK, stage, i);
+      load_ring<false>(j, stage);
     } else {
       dma_v(vb + (int64_t)(lo + j * kBK) * v_st, tile_rows(j), stage);
     }
