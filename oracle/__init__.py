@@ -4,6 +4,8 @@ TEST INFRASTRUCTURE ONLY: used by tests/, the smoke check and the benchmark's
 CPU-baseline leg.  The HIP library never imports, links or calls it."""
 from .chunk_attention import (  # noqa: F401
     attention,
+    attention_bwd,
+    attention_bwd_delta,
     brute_force,
     count_visible_pairs,
     frame_mask,

@@ -281,3 +281,59 @@ def ring_step(k_ring, v_ring, q_new, k_new, v_new, chunk_len: int, chunk_index: 
     o, lse = attention(q_new, k_seq, v_seq, chunk_len=L, q_chunk_offset=n_prev,
                        window_chunks=W, scale=scale)
     return o, lse, kr, vr
+
+
+# ---------------------------------------------------------------------------
+# Backward pass (training-mode gradients of the chunk-causal attention)
+# ---------------------------------------------------------------------------
+
+def attention_bwd(q, k, v, do, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
+                  scale: float | None = None, block: int = 512):
+    """Gradients of O = softmax(scale * Q K^T + mask) V with respect to q, k, v.
+
+    The paper trains the DiT with the whole latent sequence in parallel under
+    the chunk mask (Sec. 3.1), so training needs these gradients; the mask is
+    fixed, so it only removes terms.  Given the upstream gradient do
+    ([B, Nq, H, d]), per (b, h) with P the masked softmax weights:
+
+        dV = P^T dO
+        dP = dO V^T
+        dS = P * (dP - rowsum(dP * P))      (softmax Jacobian, row by row)
+        dQ = scale * dS K
+        dK = scale * dS^T Q
+
+    rowsum(dP * P) equals rowsum(dO * O) because O = P V.  Everything in
+    float64.  Returns (dq [B, Nq, H, d], dk [B, Nkv, H, d], dv [B, Nkv, H, d])."""
+    B, nq, H, d = q.shape
+    nkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    scale = float(scale)
+    dq = np.zeros((B, nq, H, d))
+    dk = np.zeros((B, nkv, H, d))
+    dv = np.zeros((B, nkv, H, d))
+    for b in range(B):
+        for h in range(H):
+            kh = _head_f64(k, b, h)
+            vh = _head_f64(v, b, h)
+            for r0 in range(0, nq, block):
+                rr = np.arange(r0, min(r0 + block, nq))
+                vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows=rr)
+                qh = _head_f64(q, b, h, rr)
+                doh = _head_f64(do, b, h, rr)
+                s = np.where(vis, scale * (qh @ kh.T), -np.inf)
+                p = np.exp(s - s.max(axis=1, keepdims=True))
+                p /= p.sum(axis=1, keepdims=True)
+                dp = doh @ vh.T
+                ds = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+                dq[b, rr, h] = scale * (ds @ kh)
+                dk[b, :, h] += scale * (ds.T @ qh)
+                dv[b, :, h] += p.T @ doh
+    return dq, dk, dv
+
+
+def attention_bwd_delta(o, do) -> np.ndarray:
+    """D[b, h, i] = sum_d dO[b, i, h, d] * O[b, i, h, d] (fp64), the row term of
+    the softmax backward, [B, H, Nq]."""
+    o64, do64 = _as_f64(o), _as_f64(do)
+    return np.einsum("bihd,bihd->bhi", o64, do64)

@@ -473,3 +473,89 @@ def test_ring_pins_catch_a_wrong_slot(monkeypatch):
         o_ring, _, _ = _stream_through_ring(q, k, v, 5, 1, scale=0.3)
         o_par, _ = oracle.attention(q, k, v, chunk_len=5, window_chunks=1, scale=0.3)
         np.testing.assert_allclose(o_ring, o_par, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# backward pass: gradients of the chunk-causal attention
+# ---------------------------------------------------------------------------
+
+def _loss_brute(q, k, v, do, hw, kf, W, scale):
+    """sum(dO * O) with O from the frame-level brute force of Eq. 1."""
+    o, _ = oracle.brute_force(q, k, v, hw, kf, 0, W, scale=scale)
+    return float(np.sum(do * o))
+
+
+@pytest.mark.parametrize("W", [-1, 0, 1])
+def test_bwd_matches_finite_differences_of_eq1_brute_force(W):
+    """Central differences of sum(dO * O), O from the pure-Python frame-level
+    Eq. 1, pin every gradient entry of the oracle's backward."""
+    hw, kf, T, d = 2, 2, 5, 3     # 2 tokens per latent frame, 2 frames per chunk, 5 frames
+    N, L, scale = hw * T, hw * kf, 0.7
+    rng = np.random.default_rng(100 + W)
+    q, k, v, do = (rng.standard_normal((1, N, 1, d)) for _ in range(4))
+    dq, dk, dv = oracle.attention_bwd(q, k, v, do, chunk_len=L, window_chunks=W, scale=scale)
+    eps = 1e-6
+    for name, x, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        num = np.zeros_like(x)
+        for idx in np.ndindex(*x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            args_p = dict(q=q, k=k, v=v); args_p[name] = xp
+            args_m = dict(q=q, k=k, v=v); args_m[name] = xm
+            num[idx] = (_loss_brute(args_p["q"], args_p["k"], args_p["v"], do, hw, kf, W, scale)
+                        - _loss_brute(args_m["q"], args_m["k"], args_m["v"], do, hw, kf, W, scale)) / (2 * eps)
+        np.testing.assert_allclose(g, num, rtol=0, atol=2e-8, err_msg=name)
+
+
+@pytest.mark.parametrize("W,off,nq,nkv,L", [(-1, 0, 40, 40, 8), (1, 0, 37, 37, 6), (2, 3, 10, 30, 5), (0, 0, 33, 33, 7)])
+def test_bwd_matches_autograd(W, off, nq, nkv, L):
+    """torch autograd through an explicitly masked fp64 softmax attention."""
+    B, H, d, scale = 2, 2, 8, 0.35
+    q, k, v = _rand(B, nq, nkv, H, d, seed=110 + nq)
+    do = np.random.default_rng(nq).standard_normal((B, nq, H, d))
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (q, k, v))
+    mask = torch.tensor(oracle.visibility_mask(nq, nkv, L, off, W))
+    s = torch.einsum("bihd,bjhd->bhij", tq, tk) * scale
+    s = s.masked_fill(~mask, float("-inf"))
+    o = torch.einsum("bhij,bjhd->bihd", torch.softmax(s, dim=-1), tv)
+    (o * torch.tensor(do)).sum().backward()
+    dq, dk, dv = oracle.attention_bwd(q, k, v, do, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=scale)
+    np.testing.assert_allclose(dq, tq.grad.numpy(), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dk, tk.grad.numpy(), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv, tv.grad.numpy(), rtol=0, atol=1e-11)
+
+
+def test_bwd_key_gradients_sum_to_zero_and_delta_identity():
+    """Softmax rows are shift invariant, so sum_j dS_ij = 0 and the key gradients
+    of each (b, h) sum to zero; and rowsum(dP * P) = rowsum(dO * O)."""
+    q, k, v = _rand(1, 50, 50, 2, 8, seed=120)
+    do = np.random.default_rng(5).standard_normal(q.shape)
+    dq, dk, dv = oracle.attention_bwd(q, k, v, do, chunk_len=9, window_chunks=1, scale=0.5)
+    np.testing.assert_allclose(dk.sum(axis=1), 0, atol=1e-12)
+    o, _ = oracle.attention(q, k, v, chunk_len=9, window_chunks=1, scale=0.5)
+    for h in range(2):
+        p = oracle.softmax_weights(q, k, chunk_len=9, window_chunks=1, scale=0.5, b=0, h=h)
+        dp = do[0, :, h] @ v[0, :, h].T
+        np.testing.assert_allclose((p * dp).sum(axis=1), oracle.attention_bwd_delta(o, do)[0, h], atol=1e-12)
+
+
+def test_bwd_pins_catch_a_dropped_row_term(monkeypatch):
+    """A backward without the rowsum term of the softmax Jacobian fails the
+    autograd pin."""
+    orig = oc.attention_bwd
+
+    def bad(q, k, v, do, chunk_len, q_chunk_offset=0, window_chunks=-1, scale=None, block=512):
+        B, nq, H, d = q.shape
+        dq = np.zeros_like(np.asarray(q, dtype=np.float64))
+        for b in range(B):
+            for h in range(H):
+                vis = oc.visibility_mask(nq, k.shape[1], chunk_len, q_chunk_offset, window_chunks)
+                s = np.where(vis, scale * (q[b, :, h] @ k[b, :, h].T), -np.inf)
+                p = np.exp(s - s.max(axis=1, keepdims=True)); p /= p.sum(axis=1, keepdims=True)
+                dq[b, :, h] = scale * ((p * (do[b, :, h] @ v[b, :, h].T)) @ k[b, :, h])
+        return dq, None, None
+    q, k, v = _rand(1, 20, 20, 1, 4, seed=130)
+    do = np.random.default_rng(6).standard_normal(q.shape)
+    good = orig(q, k, v, do, chunk_len=5, window_chunks=1, scale=0.5)[0]
+    assert np.abs(bad(q, k, v, do, chunk_len=5, window_chunks=1, scale=0.5)[0] - good).max() > 1e-3
