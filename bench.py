@@ -10,10 +10,11 @@ value = effective (unmasked) TFLOP/s of the whole step: 4 * d * visible pairs
 * B * H for both attention calls, divided by the step time.
 
 After the timed steps (and outside them) it reports ms/call and TFLOP/s of
-the 480p-shaped and wide sliding-window calls and of the W = 1 ring-cache
-streaming step (``other_workloads``), then the fp64 oracle baseline.
+the 480p-shaped and wide sliding-window calls, of the W = 1 ring-cache
+streaming step and of the backward of the 1080p call (``other_workloads``),
+then the fp64 oracle baseline.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
 """
 from __future__ import annotations
 
@@ -96,6 +97,27 @@ def _time_ms(torch, cur, fn, reps: int, warm: int = 2) -> float:
     return s.elapsed_time(e) / reps
 
 
+def backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, reps: int):
+    """ms/call and effective TFLOP/s of the backward (dQ, dK, dV) of the parallel
+    1080p call, given its O and LSE, for a seeded upstream gradient."""
+    from paper_2609_36757_amd.workloads import randn_bf16
+    g = torch.Generator().manual_seed(w.seed + 3000)
+    dout = randn_bf16((w.B, w.n_tokens, w.H, w.d), g).to(dev)
+    o, lse = fastvr.chunk_attn(qd, kd, vd, chunk_len=w.chunk_len, window_chunks=w.window_chunks, scale=w.scale)
+    dq = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
+    dk, dv = torch.empty_like(dq), torch.empty_like(dq)
+    rs = torch.empty((w.B, w.H, w.n_tokens, 2), dtype=torch.float32, device=dev)
+    ms = _time_ms(torch, cur, lambda: fastvr.chunk_attn_bwd(qd, kd, vd, o, lse, dout, chunk_len=w.chunk_len,
+                                                            window_chunks=w.window_chunks, scale=w.scale, dq=dq,
+                                                            dk=dk, dv=dv, row_stats=rs), reps)
+    f = 2.5 * metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
+    return {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2),
+            "frac_of_bf16_peak": round(f / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "note": "dQ, dK, dV of the parallel call given O and LSE (two kernels); effective flop = "
+                    "10 d per visible pair (5 products); the kernels execute 7 (S and dP are "
+                    "recomputed by both)"}
+
+
 def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     """ms/call and effective TFLOP/s of the other synthetic workloads: the
     480p-shaped and the wide sliding-window parallel calls, and the paper's
@@ -132,6 +154,8 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     f = metrics.effective_flops(w.B, w.H, w.d, L, 2 * L, L, 1, 1)
     res["ring_step_w1_1080p"] = {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2),
                                  "note": "chunk 3 vs chunks 2-3, append of chunk 3 fused into the launch"}
+    del ring_k, ring_v, qn, kn, vn, o, lse
+    res["bwd_1080p"] = backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, 5)
     return res
 
 
@@ -143,7 +167,9 @@ def main():
     ap.add_argument("--workload", default="1080p", choices=["1080p", "480p", "wide_sw", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2560)
-    ap.add_argument("--no-extra", action="store_true", help="skip the 480p / wide_sw / ring-step timings")
+    ap.add_argument("--no-extra", action="store_true", help="skip the 480p / wide_sw / ring-step / backward timings")
+    ap.add_argument("--bwd-only", action="store_true",
+                    help="time only the backward of the 1080p call (--steps calls) and print its figures")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build measures the single-GPU kernel "
@@ -163,6 +189,15 @@ def main():
     w = WORKLOADS[args.workload]
     q, k, v = make_sequence(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    if args.bwd_only:
+        w = WORKLOADS["1080p"]
+        if args.workload != "1080p":
+            q, k, v = make_sequence(w)
+            qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+        print(f"[bench] backward of the 1080p call: {args.steps} calls", flush=True)
+        r = backward_1080p(torch, fastvr, metrics, dev, torch.cuda.current_stream(), qd, kd, vd, w, args.steps)
+        print(json.dumps({"bwd_1080p": r}), flush=True)
+        return
     o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
 

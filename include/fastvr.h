@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 2
+#define FASTVR_ABI_VERSION 3
 
 typedef enum {
   FASTVR_OK = 0,
@@ -146,6 +146,42 @@ fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, 
                                           int64_t H, int64_t n_new, int64_t d, int64_t chunk_len,
                                           int64_t chunk_index, int64_t window_chunks, float scale,
                                           void* stream);
+
+/*
+ * Backward of fastvr_chunk_attn_fwd (gradients for training with the
+ * chunk-causal mask over the whole sequence, Sec. 3.1, Eq. 1), reusing the
+ * forward's output and LSE.  With P_ij = exp(scale * q_i . k_j - LSE_i) on
+ * visible pairs (0 elsewhere), D_i = sum_c dO_ic O_ic and
+ * dS_ij = P_ij (dO_i . v_j - D_i):
+ *   dV = P^T dO,   dQ = scale * dS K,   dK = scale * dS^T Q.
+ *
+ *   q, dout     bf16 [B, Nq,  H, d] contiguous   queries, upstream gradient dL/dO
+ *   k, v        bf16 [B, Nkv, H, d] contiguous
+ *   o           fp32 [B, Nq,  H, d] contiguous   forward output for (q, k, v)
+ *   lse         fp32 [B, H, Nq]     contiguous   forward natural-log LSE
+ *   dq          fp32 [B, Nq,  H, d] contiguous   output, fully overwritten
+ *   dk, dv      fp32 [B, Nkv, H, d] contiguous   outputs, fully overwritten (zero for
+ *                                                keys no query sees)
+ *   row_stats   fp32 [B, H, Nq, 2]  contiguous   caller-owned workspace, written by
+ *                                                the call: (LSE_i * log2 e, D_i)
+ * Mask arguments (chunk_len, q_chunk_offset, window_chunks) and scale are those
+ * of the forward call that produced o and lse.  Two kernels run in order on
+ * `stream`; sums run in a fixed order, so results are reproducible bit for bit.
+ *
+ * Preconditions (else FASTVR_ERR_INVALID_ARGUMENT unless noted):
+ *  - q, k, v, dout, o, dq, dk, dv non-NULL and 16-byte aligned (q, dout, o, dq
+ *    may be NULL when Nq = 0); lse and row_stats non-NULL and 4-byte aligned
+ *    when Nq > 0;
+ *  - dq, dk, dv and row_stats overlap no argument;
+ *  - size, offset, window and scale rules of fastvr_chunk_attn_fwd, and
+ *    H * d < 2^22 (else FASTVR_ERR_UNSUPPORTED).
+ * B, H or Nkv equal to 0 (then Nq must be 0): FASTVR_OK, nothing enqueued.
+ * Nq = 0 with Nkv > 0 sets dk and dv to zero.
+ */
+fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                                    const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
+                                    int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
+                                    int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream);
 
 /* Static string naming a status code ("FASTVR_OK", ...); never NULL. */
 const char* fastvr_status_string(fastvr_status s);

@@ -6,6 +6,7 @@ from .chunk_attention import (  # noqa: F401
     attention,
     attention_bwd,
     attention_bwd_delta,
+    attention_bwd_keys,
     brute_force,
     count_visible_pairs,
     frame_mask,

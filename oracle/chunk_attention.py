@@ -288,7 +288,7 @@ def ring_step(k_ring, v_ring, q_new, k_new, v_new, chunk_len: int, chunk_index: 
 # ---------------------------------------------------------------------------
 
 def attention_bwd(q, k, v, do, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
-                  scale: float | None = None, block: int = 512):
+                  scale: float | None = None, block: int = 512, rows=None):
     """Gradients of O = softmax(scale * Q K^T + mask) V with respect to q, k, v.
 
     The paper trains the DiT with the whole latent sequence in parallel under
@@ -303,21 +303,28 @@ def attention_bwd(q, k, v, do, chunk_len: int, q_chunk_offset: int = 0, window_c
         dK = scale * dS^T Q
 
     rowsum(dP * P) equals rowsum(dO * O) because O = P V.  Everything in
-    float64.  Returns (dq [B, Nq, H, d], dk [B, Nkv, H, d], dv [B, Nkv, H, d])."""
+    float64.  Returns (dq [B, Nq, H, d], dk [B, Nkv, H, d], dv [B, Nkv, H, d]).
+
+    rows: optional 1-D array of query rows.  Then only those rows' terms are
+    summed: dq holds the gradient of exactly those rows ([B, R, H, d]; row i of
+    dQ depends on query row i alone) and dk / dv hold those rows' contributions
+    (the full dK / dV when every query that sees a key is among the rows)."""
     B, nq, H, d = q.shape
     nkv = k.shape[1]
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     scale = float(scale)
-    dq = np.zeros((B, nq, H, d))
+    rows = np.arange(nq, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    R = rows.shape[0]
+    dq = np.zeros((B, R, H, d))
     dk = np.zeros((B, nkv, H, d))
     dv = np.zeros((B, nkv, H, d))
     for b in range(B):
         for h in range(H):
             kh = _head_f64(k, b, h)
             vh = _head_f64(v, b, h)
-            for r0 in range(0, nq, block):
-                rr = np.arange(r0, min(r0 + block, nq))
+            for r0 in range(0, R, block):
+                rr = rows[r0:r0 + block]
                 vis = visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks, rows=rr)
                 qh = _head_f64(q, b, h, rr)
                 doh = _head_f64(do, b, h, rr)
@@ -326,10 +333,55 @@ def attention_bwd(q, k, v, do, chunk_len: int, q_chunk_offset: int = 0, window_c
                 p /= p.sum(axis=1, keepdims=True)
                 dp = doh @ vh.T
                 ds = p * (dp - (p * dp).sum(axis=1, keepdims=True))
-                dq[b, rr, h] = scale * (ds @ kh)
+                dq[b, r0:r0 + len(rr), h] = scale * (ds @ kh)
                 dk[b, :, h] += scale * (ds.T @ qh)
                 dv[b, :, h] += p.T @ doh
     return dq, dk, dv
+
+
+def attention_bwd_keys(q, k, v, do, keys, lse, delta, chunk_len: int, q_chunk_offset: int = 0,
+                       window_chunks: int = -1, scale: float | None = None):
+    """dK and dV of the key rows ``keys`` only, from the per-query row terms.
+
+    For key j, with the queries i that see it (Eq. 1 mask):
+        P_ij  = exp(scale * q_i . k_j - LSE_i)
+        dS_ij = P_ij * (dO_i . v_j - D_i)
+        dV_j  = sum_i P_ij dO_i,      dK_j = scale * sum_i dS_ij q_i
+    lse and delta are [B, H, Nq] (LSE_i and D_i = rowsum(dO * O)_i, e.g. from
+    ``attention`` and ``attention_bwd_delta``); entries of queries that see none
+    of the keys are never read.  Returns (dk, dv), each [B, len(keys), H, d],
+    float64."""
+    B, nq, H, d = q.shape
+    nkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    scale = float(scale)
+    keys = np.asarray(keys, dtype=np.int64)
+    cq = query_chunks(nq, chunk_len, q_chunk_offset)
+    ck = key_chunks(nkv, chunk_len)[keys]
+    diff = cq[None, :] - ck[:, None]                      # [K, Nq]
+    vis = diff >= 0
+    if window_chunks >= 0:
+        vis &= diff <= window_chunks
+    lse = np.asarray(lse, dtype=np.float64)
+    delta = np.asarray(delta, dtype=np.float64)
+    dk = np.zeros((B, len(keys), H, d))
+    dv = np.zeros((B, len(keys), H, d))
+    for b in range(B):
+        for h in range(H):
+            for t, j in enumerate(keys):
+                ii = np.nonzero(vis[t])[0]
+                if ii.size == 0:
+                    continue
+                qh = _head_f64(q, b, h, ii)
+                doh = _head_f64(do, b, h, ii)
+                kj = _head_f64(k, b, h, np.array([j]))[0]
+                vj = _head_f64(v, b, h, np.array([j]))[0]
+                p = np.exp(scale * (qh @ kj) - lse[b, h, ii])
+                ds = p * (doh @ vj - delta[b, h, ii])
+                dv[b, t, h] = p @ doh
+                dk[b, t, h] = scale * (ds @ qh)
+    return dk, dv
 
 
 def attention_bwd_delta(o, do) -> np.ndarray:

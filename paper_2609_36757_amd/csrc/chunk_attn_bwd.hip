@@ -1,0 +1,613 @@
+// Chunk-wise causal attention backward for CDNA4 (gfx950).
+//
+// Gradients of O = softmax(scale * Q K^T + M) V (FastVR, Sec. 3.1, Eq. 1; M the
+// chunk-causal mask) for an upstream gradient dO, reusing the forward's LSE:
+//   P   = exp(scale * Q K^T - LSE)            recomputed per tile, never stored
+//   D_i = sum_d dO_id * O_id
+//   dV  = P^T dO,   dP = dO V^T,   dS = P o (dP - D),
+//   dQ  = scale * dS K,   dK = scale * dS^T Q.
+// As in the forward, the keys a query chunk sees form one contiguous interval
+// and the queries that see a key chunk form one contiguous interval, so masked
+// chunk pairs are never visited.
+//
+// Two kernels, no atomics, so every gradient is a fixed-order sum (results are
+// reproducible bit for bit):
+//  * dQ kernel (query-stationary, the forward's grid): 8 waves, 32 queries each,
+//    Q and dO fragments in registers.  It first writes (LSE * log2 e, D) of its
+//    rows to a workspace, then per 64-key tile computes S^T = K Q^T and
+//    dP^T = V dO^T (one query per lane, 16 keys per lane), P^T and dS^T in
+//    registers, and dQ^T += K^T dS^T.
+//  * dK/dV kernel (key-stationary): a workgroup owns 128 keys of one chunk
+//    (4 waves, 32 keys each, K and V fragments in registers) and walks the
+//    64-query tiles of the queries that see that chunk: S = Q K^T and
+//    dP = dO V^T (one key per lane, 16 queries per lane), then
+//    dV^T += dO^T P and dK^T += Q^T dS.  Both accumulators stay in registers
+//    (one wave per SIMD).
+// All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation; P and dS
+// are rounded to bf16 as MFMA operands.
+//
+// Streamed tiles (K and V, or Q and dO: 64 rows of d bf16) travel by DMA from
+// HBM straight into LDS (buffer_load ... lds), triple-buffered and issued two
+// tiles ahead.  Every row offset is in the per-lane VGPR offset, which the
+// buffer range check covers, so rows past a tile's valid end read as zero.
+// In LDS a row keeps its 16-byte chunks with the chunk index XOR bswz(row);
+// the same tile is read both by rows (ds_read_b128, MFMA operands K, V, Q, dO)
+// and transposed (ds_read_b64_tr_b16, operands K^T, Q^T, dO^T), and bswz keeps
+// both free of LDS bank conflicts.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gfx950_ops.h"
+#include "launch.h"
+
+namespace fastvr {
+namespace {
+
+using namespace dev;
+
+constexpr int kTile = 64;  // rows per staged tile: keys (dQ) or queries (dK/dV)
+constexpr int kStages = 3;
+constexpr int kDqWaves = kBwdDqThreads / 64;    // 8
+constexpr int kDkvWaves = kBwdDkvThreads / 64;  // 4
+constexpr int kDqRows = 32 * kDqWaves;          // 256 queries per dQ workgroup
+static_assert(kDqRows == kFwdRowsPerItem, "the dQ grid is the forward's");
+static_assert(32 * kDkvWaves == kBwdKeysPerItem, "32 keys per dK/dV wave");
+
+struct BwdParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint16_t* dout;
+  const float* o;
+  const float* lse;
+  float* dq;
+  float* dk;
+  float* dv;
+  float* rs;             // row statistics [B, H, nq, 2]
+  int64_t q_sb, kv_sb;   // batch strides (elements) of the query-side and key-side tensors
+  int32_t st;            // token stride H * d (elements), all tensors
+  int32_t nq, nkv, chunk_len, q_chunk_offset, window;  // window -1 = unbounded
+  int32_t B, H;
+  int32_t n_local_chunks, tiles_full, tiles_last, n_q_items;
+  int32_t n_kchunks, kblocks_full, kblocks_last, n_kv_items;
+  float c;      // scale * log2(e)
+  float scale;
+};
+
+// XOR applied to the 16-byte chunk index of row r of a staged tile.
+//  * Row reads: 16 lanes read one logical chunk of 16 consecutive rows, so
+//    bswz must be one-to-one on r mod 16 (d = 128: a row is one 256-byte bank
+//    row of 16 chunk slots; d = 64: two rows share a bank row, one-to-one per
+//    row parity).
+//  * Transposed reads: 32 lanes read rows 4a .. 4a+3 and logical chunks
+//    4m .. 4m+3, so the four rows must fall into four different chunk quads
+//    (d = 128), or two per row parity (d = 64).
+template <int D>
+__device__ __forceinline__ int bswz(int r) {
+  return D >= 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
+// Staged tile of 64 rows x D bf16 filled by NW waves.
+template <int D, int NW>
+struct TileDma {
+  static constexpr int kChunks = D / 8;                    // 16-byte chunks per row
+  static constexpr int kElems = kTile * D;                 // bf16 per stage
+  static constexpr int kRowsPerInst = 64 / kChunks;        // rows one wave instruction fills
+  static constexpr int kPer = kTile * kChunks / (64 * NW); // instructions per wave per tile
+  static_assert(kPer >= 1 && (NW * kRowsPerInst) % 16 == 0, "row swizzle must repeat per instruction");
+  uint32_t off;   // this lane's byte offset in the source tile, instruction 0
+  uint32_t step;  // byte offset between consecutive instructions
+
+  // Instruction i of wave w fills LDS chunk slots (i * NW + w) * 64 + lane: row
+  // P / kChunks, physical chunk P % kChunks, read from logical chunk
+  // phys ^ bswz(row).  Rows advance by NW * kRowsPerInst (a multiple of 16)
+  // per instruction, so the swizzle of a lane's row does not depend on i.
+  __device__ __forceinline__ void init(int wave, int lane, int st) {
+    const int P = wave * 64 + lane;
+    const int row = P / kChunks, phys = P % kChunks;
+    off = (uint32_t)(row * st + (phys ^ bswz<D>(row)) * 8) * 2u;
+    step = (uint32_t)(NW * kRowsPerInst * st) * 2u;
+  }
+  // DMA of a tile whose first row is `base` and whose `rows` first rows are
+  // valid (rows past them, all of them when rows <= 0, read as zero).
+  __device__ __forceinline__ void load(const uint16_t* base, int rows, int st, uint16_t* dst, int wave) const {
+    const i32x4 rsrc = make_vsharp(base, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    const uint32_t la = lds_addr(dst) + (uint32_t)(wave * 64 * 16);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) dma16(la + (uint32_t)(i * NW * 64 * 16), off + (uint32_t)i * step, rsrc, 0);
+  }
+};
+
+// Operand reads from a staged tile, for lane (n = lane % 32, hh = lane / 32).
+template <int D>
+struct TileReads {
+  int row_rd[D / 16];     // row reads: row n, logical chunk 2 kk + hh
+  int tr_rd[D / 32][2];   // transposed reads, rows 4 hh + (i >> 2) (+ 8)
+
+  __device__ __forceinline__ void init(int lane) {
+    const int n = lane & 31, hh = lane >> 5;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) row_rd[kk] = n * (D * 2) + (((2 * kk + hh) ^ bswz<D>(n)) * 16);
+    // 16-lane block b = lane / 16, i = lane % 16: the lane addresses row
+    // 4 hh + (i >> 2) (and 8 rows further), dims dm * 32 + 16 (b & 1) + 4 (i & 3)
+    // .. + 3, and receives rows 4 hh + 0..3 of dim dm * 32 + 16 (b & 1) + i.
+    const int i = lane & 15, b = lane >> 4;
+#pragma unroll
+    for (int dm = 0; dm < D / 32; ++dm)
+#pragma unroll
+      for (int h8 = 0; h8 < 2; ++h8) {
+        const int row = hh * 4 + (i >> 2) + 8 * h8;
+        const int logical = dm * 4 + 2 * (b & 1) + ((i >> 1) & 1);
+        tr_rd[dm][h8] = row * (D * 2) + ((logical ^ bswz<D>(row)) * 16) + (i & 1) * 8;
+      }
+  }
+  // A operand rows mb * 32 + n, dims 16 kk + 8 hh .. + 7
+  __device__ __forceinline__ u32x4 row(const char* t, int mb, int kk) const {
+    return *reinterpret_cast<const u32x4*>(t + row_rd[kk] + mb * 32 * (D * 2));
+  }
+  // A operand of T^T for k-step g (tile rows 16 g .. 16 g + 15) and dims
+  // dm * 32 .. + 31: lane (i_A, hh) gets T[16 g + 4 hh + {0..3, 8..11}][dm * 32 + i_A]
+  __device__ __forceinline__ u32x4 tr(const char* t, int g, int dm) const {
+    const char* base = t + g * 16 * (D * 2);
+    const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + tr_rd[dm][0]));
+    const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + tr_rd[dm][1]));
+    return __builtin_bit_cast(u32x4, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
+};
+
+// bf16 B-operand fragments of a 32-row accumulator a (rows 8 (v >> 2) +
+// 4 hh + (v & 3)): k-step gg covers rows 16 gg .. 16 gg + 15 in the order the
+// transposed reads deliver them.
+__device__ __forceinline__ void pack_bf16_half(const f32x16& a, u32x4 (&f)[2]) {
+#pragma unroll
+  for (int gg = 0; gg < 2; ++gg) {
+    bf16x8 b;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) b[r] = (__bf16)a[8 * gg + r];
+    f[gg] = __builtin_bit_cast(u32x4, b);
+  }
+}
+// The same for a 64-row pair a[0], a[1] (rows 32 mb + ...): k-step g covers
+// rows 16 g .. 16 g + 15.
+__device__ __forceinline__ void pack_bf16(const f32x16 (&a)[2], u32x4 (&f)[4]) {
+  u32x4 f0[2], f1[2];
+  pack_bf16_half(a[0], f0);
+  pack_bf16_half(a[1], f1);
+  f[0] = f0[0];
+  f[1] = f0[1];
+  f[2] = f1[0];
+  f[3] = f1[1];
+}
+
+// Workgroups go to the 8 XCDs round-robin; within each full round of 256,
+// XCD x gets 32 consecutive items (neighbouring tiles of one stream share its L2).
+__device__ __forceinline__ int xcd_item(int i, int n_items) {
+  constexpr int kRound = 256;
+  const int full = (n_items / kRound) * kRound;
+  if (i >= full) return i;
+  const int r = i / kRound, w = i % kRound;
+  return r * kRound + (w & 7) * 32 + (w >> 3);
+}
+
+// ---------------------------------------------------------------- dQ kernel
+
+template <int D>
+__global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const BwdParams p) {
+  using Dma = TileDma<D, kDqWaves>;
+  constexpr int kStage = Dma::kElems;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStages * kStage];
+  uint16_t* ks = smem;
+  uint16_t* vs = smem + kStages * kStage;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, hh = lane >> 5;
+
+  // item -> (local query chunk, batch*head, tile), last chunk first (longest)
+  int cl, bh, t;
+  {
+    const int vi = xcd_item(blockIdx.x, p.n_q_items);
+    const int BH = p.B * p.H;
+    const int n_last = BH * p.tiles_last;
+    if (vi < n_last) {
+      cl = p.n_local_chunks - 1;
+      bh = vi / p.tiles_last;
+      t = vi - bh * p.tiles_last;
+    } else {
+      const int v2 = vi - n_last;
+      const int per = BH * p.tiles_full;
+      const int rank = v2 / per;
+      const int rem = v2 - rank * per;
+      cl = p.n_local_chunks - 2 - rank;
+      bh = rem / p.tiles_full;
+      t = rem - bh * p.tiles_full;
+    }
+  }
+  const int b = bh / p.H, h = bh - (bh / p.H) * p.H;
+  const int L = p.chunk_len;
+  const int chunk_q0 = cl * L;
+  const int q_end = (L < p.nq - chunk_q0) ? chunk_q0 + L : p.nq;
+  const int q0 = chunk_q0 + t * kDqRows;
+  const int cg = p.q_chunk_offset + cl;
+  const int lo = (p.window >= 0 && cg > p.window) ? (cg - p.window) * L : 0;
+  const int hi = (L < p.nkv - cg * L) ? (cg + 1) * L : p.nkv;
+  const int n_tiles = (hi - lo + kTile - 1) / kTile;
+  const int st = p.st;
+  const uint16_t* kb = p.k + (int64_t)b * p.kv_sb + (int64_t)h * D;
+  const uint16_t* vb = p.v + (int64_t)b * p.kv_sb + (int64_t)h * D;
+
+  Dma dma;
+  dma.init(wave, lane, st);
+  TileReads<D> rd;
+  rd.init(lane);
+  auto tile_rows = [&](int j) { return hi - (lo + j * kTile); };
+
+  // prologue: K and V tiles 0 and 1 to LDS
+  dma.load(kb + (int64_t)lo * st, tile_rows(0), st, ks, wave);
+  dma.load(vb + (int64_t)lo * st, tile_rows(0), st, vs, wave);
+  dma.load(kb + (int64_t)(lo + kTile) * st, tile_rows(1), st, ks + kStage, wave);
+  dma.load(vb + (int64_t)(lo + kTile) * st, tile_rows(1), st, vs + kStage, wave);
+
+  // this wave's 32 query rows: Q and dO fragments (B operands Q^T, dO^T), the
+  // row statistics, written to the workspace for the dK/dV kernel
+  const int row = q0 + wave * 32 + n;
+  const bool row_ok = row < q_end;
+  u32x4 qf[D / 16], dof[D / 16];
+  float lse2, dlt;
+  {
+    const int rows = q_end - (q0 + wave * 32);  // valid rows of this wave (may be <= 0)
+    const int64_t qoff = (int64_t)b * p.q_sb + (int64_t)(q0 + wave * 32) * st + (int64_t)h * D;
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc(p.q + qoff, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rdo = make_rsrc(p.dout + qoff, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(p.o + qoff, rows > 0 ? (int64_t)rows * st * 4 : 0);
+    float dpart = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const uint32_t e = (uint32_t)(n * st + kk * 16 + hh * 8);  // element offset of dims 16 kk + 8 hh
+      qf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, e * 2u, 0, 0));
+      dof[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rdo, e * 2u, 0, 0));
+      const f32x4 o0 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, e * 4u, 0, 0));
+      const f32x4 o1 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, e * 4u + 16u, 0, 0));
+      const bf16x8 d8 = __builtin_bit_cast(bf16x8, dof[kk]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        dpart = __builtin_fmaf((float)d8[r], o0[r], dpart);
+        dpart = __builtin_fmaf((float)d8[4 + r], o1[r], dpart);
+      }
+    }
+    float dother;
+    const float dmine = swap_halves(dpart, &dother);
+    dlt = dmine + dother;  // the same sum in both halves
+    const float lse = row_ok ? p.lse[((int64_t)b * p.H + h) * p.nq + row] : 0.f;
+    lse2 = row_ok ? lse * 1.44269504088896340736f : 0.f;
+    dlt = row_ok ? dlt : 0.f;
+    if (row_ok && hh == 0) {
+      float* rs = p.rs + (((int64_t)b * p.H + h) * p.nq + row) * 2;
+      rs[0] = lse2;
+      rs[1] = dlt;
+    }
+  }
+  f32x16 acc[D / 32];
+#pragma unroll
+  for (int dm = 0; dm < D / 32; ++dm) acc[dm] = f32x16{};
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  barrier();
+
+  const float c = p.c;
+  const int last_valid = hi - (lo + (n_tiles - 1) * kTile);
+  int s_cur = 0, s_next = 1, s_free = 2;
+  for (int j = 0; j < n_tiles; ++j) {
+    // tile j + 2 into the stage tile j - 1 used (zero rows past the interval)
+    dma.load(kb + (int64_t)(lo + (j + 2) * kTile) * st, tile_rows(j + 2), st, ks + s_free * kStage, wave);
+    dma.load(vb + (int64_t)(lo + (j + 2) * kTile) * st, tile_rows(j + 2), st, vs + s_free * kStage, wave);
+    const char* kst = reinterpret_cast<const char*>(ks + s_cur * kStage);
+    const char* vst = reinterpret_cast<const char*>(vs + s_cur * kStage);
+    // The tile's two 32-key halves one after the other (register budget of
+    // two waves per SIMD).
+    const int lim = (j + 1 == n_tiles) ? last_valid - 4 * hh : kTile;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      // S^T = K Q^T and dP^T = V dO^T: lane = query n, 16 keys per lane
+      f32x16 s, dp;
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) {
+        s = mfma32(rd.row(kst, mb, kk), qf[kk], kk == 0 ? f32x16{} : s);
+        dp = mfma32(rd.row(vst, mb, kk), dof[kk], kk == 0 ? f32x16{} : dp);
+      }
+      // P^T = exp2(S^T c - LSE log2 e); dS^T = P^T (dP^T - D).  Keys past the
+      // interval (last tile only) get P = 0.
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = mb * 32 + 8 * (v >> 2) + (v & 3);
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c, -lse2));
+        pv = key < lim ? pv : 0.f;
+        s[v] = pv * (dp[v] - dlt);
+      }
+      u32x4 dsf[2];
+      pack_bf16_half(s, dsf);
+      // dQ^T += K^T dS^T over keys 32 mb .. 32 mb + 31
+#pragma unroll
+      for (int gg = 0; gg < 2; ++gg)
+#pragma unroll
+        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(kst, 2 * mb + gg, dm), dsf[gg], acc[dm]);
+    }
+    wait_vmcnt<2 * Dma::kPer>();
+    barrier();
+    const int s_old = s_cur;
+    s_cur = s_next;
+    s_next = s_free;
+    s_free = s_old;
+  }
+  wait_vmcnt<0>();
+
+  // dQ = scale * dQ^T: lane n holds dims dm * 32 + 8 g + 4 hh + 0..3 of its row
+  if (row_ok) {
+    float* out = p.dq + (int64_t)b * p.q_sb + (int64_t)row * st + (int64_t)h * D;
+    const float sc = p.scale;
+#pragma unroll
+    for (int dm = 0; dm < D / 32; ++dm)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 val;
+        val.x = acc[dm][4 * g + 0] * sc;
+        val.y = acc[dm][4 * g + 1] * sc;
+        val.z = acc[dm][4 * g + 2] * sc;
+        val.w = acc[dm][4 * g + 3] * sc;
+        *reinterpret_cast<f32x4*>(out + dm * 32 + g * 8 + hh * 4) = val;
+      }
+  }
+}
+
+// -------------------------------------------------------------- dK/dV kernel
+
+template <int D>
+__global__ __launch_bounds__(kBwdDkvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void
+chunk_attn_bwd_dkv_kernel(const BwdParams p) {
+  using Dma = TileDma<D, kDkvWaves>;
+  constexpr int kStage = Dma::kElems;
+  constexpr int kRsFloats = 2 * kTile;  // (LSE log2 e, D) of the tile's 64 queries
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStages * kStage];
+  __shared__ __attribute__((aligned(16))) float rss[kStages * kRsFloats];
+  uint16_t* qs = smem;
+  uint16_t* dos = smem + kStages * kStage;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lane & 31, hh = lane >> 5;
+
+  // item -> (key chunk, batch*head, key block), first chunk first: with an
+  // unbounded window the earliest keys are seen by the most queries
+  int ck, bh, kblk;
+  {
+    const int vi = xcd_item(blockIdx.x, p.n_kv_items);
+    const int BH = p.B * p.H;
+    const int n_full = (p.n_kchunks - 1) * BH * p.kblocks_full;
+    if (vi < n_full) {
+      const int per = BH * p.kblocks_full;
+      ck = vi / per;
+      const int rem = vi - ck * per;
+      bh = rem / p.kblocks_full;
+      kblk = rem - bh * p.kblocks_full;
+    } else {
+      const int v2 = vi - n_full;
+      ck = p.n_kchunks - 1;
+      bh = v2 / p.kblocks_last;
+      kblk = v2 - bh * p.kblocks_last;
+    }
+  }
+  const int b = bh / p.H, h = bh - (bh / p.H) * p.H;
+  const int L = p.chunk_len;
+  const int key_end = (L < p.nkv - ck * L) ? (ck + 1) * L : p.nkv;
+  const int key0 = ck * L + kblk * kBwdKeysPerItem + wave * 32;  // this wave's first key
+  const int key = key0 + n;
+  // queries that see key chunk ck: local chunks [ck - q_off, ck + W - q_off]
+  int cl_lo = ck - p.q_chunk_offset;
+  if (cl_lo < 0) cl_lo = 0;
+  int cl_hi = p.n_local_chunks;  // exclusive
+  if (p.window >= 0 && ck + p.window - p.q_chunk_offset + 1 < cl_hi) cl_hi = ck + p.window - p.q_chunk_offset + 1;
+  const int qlo = cl_lo * L;
+  int qhi = cl_hi * L;
+  if (qhi > p.nq) qhi = p.nq;
+  const int n_tiles = qhi > qlo ? (qhi - qlo + kTile - 1) / kTile : 0;
+  const int st = p.st;
+  const uint16_t* qb = p.q + (int64_t)b * p.q_sb + (int64_t)h * D;
+  const uint16_t* dob = p.dout + (int64_t)b * p.q_sb + (int64_t)h * D;
+  const float* rsb = p.rs + ((int64_t)b * p.H + h) * p.nq * 2;
+
+  Dma dma;
+  dma.init(wave, lane, st);
+  TileReads<D> rd;
+  rd.init(lane);
+  auto tile_rows = [&](int j) { return qhi - (qlo + j * kTile); };
+  // row statistics of tile j: 64 pairs = 128 floats, 4 bytes per lane from the
+  // first 32 lanes of each wave (exec-masked; the tile may start at an odd
+  // row, so 16-byte units could be misaligned), zero past the query range
+  auto load_rs = [&](int j, int stage) {
+    if (lane < 32) {
+      const int rows = tile_rows(j);
+      const i32x4 rsrc = make_vsharp(rsb + (int64_t)(qlo + j * kTile) * 2, rows > 0 ? (int64_t)rows * 8 : 0);
+      const uint32_t la = lds_addr(rss + stage * kRsFloats) + (uint32_t)(wave * 32 * 4);
+      dma4(la, (uint32_t)((wave * 32 + lane) * 4), rsrc, 0);
+    }
+  };
+  auto load_tile = [&](int j, int stage) {
+    dma.load(qb + (int64_t)(qlo + j * kTile) * st, tile_rows(j), st, qs + stage * kStage, wave);
+    dma.load(dob + (int64_t)(qlo + j * kTile) * st, tile_rows(j), st, dos + stage * kStage, wave);
+    load_rs(j, stage);
+  };
+  if (n_tiles > 0) {
+    load_tile(0, 0);
+    load_tile(1, 1);
+  }
+
+  // K and V fragments (B operands K^T, V^T) of this wave's 32 keys
+  u32x4 kf[D / 16], vf[D / 16];
+  {
+    const int rows = key_end - key0;
+    const int64_t koff = (int64_t)b * p.kv_sb + (int64_t)key0 * st + (int64_t)h * D;
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + koff, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + koff, rows > 0 ? (int64_t)rows * st * 2 : 0);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const uint32_t e = (uint32_t)(n * st + kk * 16 + hh * 8);
+      kf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, e * 2u, 0, 0));
+      vf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, e * 2u, 0, 0));
+    }
+  }
+  f32x16 dka[D / 32], dva[D / 32];
+#pragma unroll
+  for (int dm = 0; dm < D / 32; ++dm) {
+    dka[dm] = f32x16{};
+    dva[dm] = f32x16{};
+  }
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  barrier();
+
+  const float c = p.c;
+  int s_cur = 0, s_next = 1, s_free = 2;
+  for (int j = 0; j < n_tiles; ++j) {
+    load_tile(j + 2, s_free);
+    const char* qst = reinterpret_cast<const char*>(qs + s_cur * kStage);
+    const char* dost = reinterpret_cast<const char*>(dos + s_cur * kStage);
+    const float* rst = rss + s_cur * kRsFloats;
+    f32x16 s[2], dp[2];
+    // S = Q K^T and dP = dO V^T: lane = key n, 16 queries per lane
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) s[mb] = mfma32(rd.row(qst, mb, kk), kf[kk], kk == 0 ? f32x16{} : s[mb]);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) dp[mb] = mfma32(rd.row(dost, mb, kk), vf[kk], kk == 0 ? f32x16{} : dp[mb]);
+    // P = exp2(S c - LSE log2 e), dS = P (dP - D) per query row
+    // 32 mb + 8 g + 4 hh + r; rows past the query range have Q = dO = 0 and
+    // zero statistics, so P = 1 and dS = 0 there and they add nothing
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4* rp = reinterpret_cast<const f32x4*>(rst + 2 * (32 * mb + 8 * g + 4 * hh));
+        const f32x4 r01 = rp[0], r23 = rp[1];  // (lse2, D) of rows +0, +1 and +2, +3
+        const float l2[4] = {r01.x, r01.z, r23.x, r23.z};
+        const float dd[4] = {r01.y, r01.w, r23.y, r23.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int v = 4 * g + r;
+          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][v], c, -l2[r]));
+          s[mb][v] = pv;
+          dp[mb][v] = pv * (dp[mb][v] - dd[r]);
+        }
+      }
+    u32x4 pf[4], dsf[4];
+    pack_bf16(s, pf);
+    pack_bf16(dp, dsf);
+    // dV^T += dO^T P and dK^T += Q^T dS
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int dm = 0; dm < D / 32; ++dm) dva[dm] = mfma32(rd.tr(dost, g, dm), pf[g], dva[dm]);
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int dm = 0; dm < D / 32; ++dm) dka[dm] = mfma32(rd.tr(qst, g, dm), dsf[g], dka[dm]);
+    wait_vmcnt<2 * Dma::kPer + 1>();
+    barrier();
+    const int s_old = s_cur;
+    s_cur = s_next;
+    s_next = s_free;
+    s_free = s_old;
+  }
+  wait_vmcnt<0>();
+
+  // dK = scale * dK^T, dV = dV^T: lane n holds dims dm * 32 + 8 g + 4 hh + 0..3 of key n
+  if (key < key_end) {
+    const int64_t off = (int64_t)b * p.kv_sb + (int64_t)key * st + (int64_t)h * D;
+    float* dko = p.dk + off;
+    float* dvo = p.dv + off;
+    const float sc = p.scale;
+#pragma unroll
+    for (int dm = 0; dm < D / 32; ++dm)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 kv, vv;
+        kv.x = dka[dm][4 * g + 0] * sc;
+        kv.y = dka[dm][4 * g + 1] * sc;
+        kv.z = dka[dm][4 * g + 2] * sc;
+        kv.w = dka[dm][4 * g + 3] * sc;
+        vv.x = dva[dm][4 * g + 0];
+        vv.y = dva[dm][4 * g + 1];
+        vv.z = dva[dm][4 * g + 2];
+        vv.w = dva[dm][4 * g + 3];
+        *reinterpret_cast<f32x4*>(dko + dm * 32 + g * 8 + hh * 4) = kv;
+        *reinterpret_cast<f32x4*>(dvo + dm * 32 + g * 8 + hh * 4) = vv;
+      }
+  }
+}
+
+template <int D>
+hipError_t launch_bwd_t(const BwdParams& p, hipStream_t stream) {
+  if (p.n_q_items > 0)
+    hipLaunchKernelGGL((chunk_attn_bwd_dq_kernel<D>), dim3((unsigned)p.n_q_items), dim3(kBwdDqThreads), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (p.n_kv_items > 0)
+    hipLaunchKernelGGL((chunk_attn_bwd_dkv_kernel<D>), dim3((unsigned)p.n_kv_items), dim3(kBwdDkvThreads), 0, stream,
+                       p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len) {
+  BwdGrid g{};
+  const int64_t L = chunk_len > nkv ? nkv : chunk_len;
+  g.q = fwd_grid(B, H, nq, L);
+  if (B <= 0 || H <= 0 || nkv <= 0 || L <= 0) return g;
+  g.n_kchunks = (nkv + L - 1) / L;
+  const int64_t last_keys = nkv - (g.n_kchunks - 1) * L;
+  g.kblocks_last = (last_keys + kBwdKeysPerItem - 1) / kBwdKeysPerItem;
+  g.kblocks_full = g.n_kchunks > 1 ? (L + kBwdKeysPerItem - 1) / kBwdKeysPerItem : g.kblocks_last;
+  g.n_kv_items = B * H * (g.kblocks_last + g.kblocks_full * (g.n_kchunks - 1));
+  return g;
+}
+
+hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream) {
+  const BwdGrid g = bwd_grid(a.B, a.H, a.nq, a.nkv, a.chunk_len);
+  BwdParams p;
+  p.q = static_cast<const uint16_t*>(a.q);
+  p.k = static_cast<const uint16_t*>(a.k);
+  p.v = static_cast<const uint16_t*>(a.v);
+  p.dout = static_cast<const uint16_t*>(a.dout);
+  p.o = a.o;
+  p.lse = a.lse;
+  p.dq = a.dq;
+  p.dk = a.dk;
+  p.dv = a.dv;
+  p.rs = a.row_stats;
+  p.st = (int32_t)(a.H * a.d);
+  p.q_sb = a.nq * a.H * a.d;
+  p.kv_sb = a.nkv * a.H * a.d;
+  // a chunk longer than the key range (only with q_chunk_offset = 0) is the
+  // same as a chunk of exactly Nkv tokens
+  const int64_t L = (a.chunk_len > a.nkv) ? a.nkv : a.chunk_len;
+  p.nq = (int32_t)a.nq;
+  p.nkv = (int32_t)a.nkv;
+  p.chunk_len = (int32_t)L;
+  p.q_chunk_offset = (int32_t)a.q_chunk_offset;
+  p.window = (int32_t)((a.window_chunks < 0 || a.window_chunks > a.nkv) ? -1 : a.window_chunks);
+  p.B = (int32_t)a.B;
+  p.H = (int32_t)a.H;
+  p.n_local_chunks = (int32_t)g.q.n_local_chunks;
+  p.tiles_full = (int32_t)g.q.tiles_full;
+  p.tiles_last = (int32_t)g.q.tiles_last;
+  p.n_q_items = (int32_t)g.q.n_items;
+  p.n_kchunks = (int32_t)g.n_kchunks;
+  p.kblocks_full = (int32_t)g.kblocks_full;
+  p.kblocks_last = (int32_t)g.kblocks_last;
+  p.n_kv_items = (int32_t)g.n_kv_items;
+  p.c = a.scale * 1.44269504088896340736f;
+  p.scale = a.scale;
+  if (a.d == 128) return launch_bwd_t<128>(p, stream);
+  return launch_bwd_t<64>(p, stream);
+}
+
+}  // namespace fastvr

@@ -256,6 +256,97 @@ fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, 
                   n_prev, window_chunks, scale, stream, r);
 }
 
+fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                                    const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
+                                    int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
+                                    int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+  if (B < 0 || H < 0 || Nq < 0 || Nkv < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld H=%lld Nq=%lld Nkv=%lld)", (long long)B,
+                (long long)H, (long long)Nq, (long long)Nkv);
+  if (d != 64 && d != 128) return fail(FASTVR_ERR_UNSUPPORTED, "head_dim %lld not in {64, 128}", (long long)d);
+  if (q_chunk_offset < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "q_chunk_offset %lld < 0", (long long)q_chunk_offset);
+  if (window_chunks < -1)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "window_chunks %lld < -1", (long long)window_chunks);
+  if (!std::isfinite(scale)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "scale is not finite");
+  if (B == 0 || H == 0 || Nkv == 0) {
+    if (Nq > 0 && B > 0 && H > 0)
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "Nq = %lld queries but no keys", (long long)Nq);
+    return ok();  // nothing to write
+  }
+  if (chunk_len < 1) return fail(FASTVR_ERR_INVALID_ARGUMENT, "chunk_len %lld < 1", (long long)chunk_len);
+  int64_t first_q, last_q;
+  if (!mul_ok(q_chunk_offset, chunk_len, &first_q) || !add_ok(first_q, Nq, &last_q))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "q_chunk_offset * chunk_len + Nq overflows int64");
+  if (last_q > Nkv)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT,
+                "q_chunk_offset * chunk_len + Nq = %lld > Nkv = %lld (a query would not see its own key)",
+                (long long)last_q, (long long)Nkv);
+  if (Nkv > INT32_MAX || Nq > INT32_MAX || B > INT32_MAX || H > INT32_MAX)
+    return fail(FASTVR_ERR_UNSUPPORTED, "sizes must be below 2^31");
+  int64_t hd, bh, nrows;
+  if (!mul_ok(H, d, &hd) || !mul_ok(B, H, &bh) || !mul_ok(bh, Nq, &nrows))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  if (hd >= fastvr::kMaxTokenStride)
+    return fail(FASTVR_ERR_UNSUPPORTED, "H * d = %lld must be below %lld", (long long)hd,
+                (long long)fastvr::kMaxTokenStride);
+  int64_t sq, skv;
+  if (!mul_ok(Nq, hd, &sq) || !mul_ok(Nkv, hd, &skv)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  // every tensor is contiguous; views give the byte extents for the overlap checks
+  const View views[8] = {{"q", q, sq, hd, Nq, 2},         {"dout", dout, sq, hd, Nq, 2},
+                         {"o", o, sq, hd, Nq, 4},         {"dq", dq, sq, hd, Nq, 4},
+                         {"k", k, skv, hd, Nkv, 2},       {"v", v, skv, hd, Nkv, 2},
+                         {"dk", dk, skv, hd, Nkv, 4},     {"dv", dv, skv, hd, Nkv, 4}};
+  int64_t bytes[10] = {0};
+  fastvr_status s;
+  for (int i = 0; i < 8; ++i) {
+    if (views[i].n == 0) {
+      // Nq = 0: the query-side tensors are not read; dK and dV become zero
+      if (views[i].ptr != nullptr && !aligned(views[i].ptr, 16))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", views[i].name);
+      continue;
+    }
+    if ((s = check_view(views[i], B, hd, &bytes[i])) != FASTVR_OK) return s;
+  }
+  const void* lse_ptr = lse;
+  const void* rs_ptr = row_stats;
+  if (Nq > 0) {
+    if (lse == nullptr || row_stats == nullptr)
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is NULL");
+    if (!aligned(lse, 4) || !aligned(row_stats, 4))
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is not 4-byte aligned");
+    if (!mul_ok(nrows, 4, &bytes[8]) || !mul_ok(nrows, 8, &bytes[9]))
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  }
+  // outputs (dq, dk, dv, row_stats) overlap nothing else
+  const void* ptrs[10] = {q, dout, o, dq, k, v, dk, dv, lse_ptr, rs_ptr};
+  const int outs[4] = {3, 6, 7, 9};
+  for (int oi = 0; oi < 4; ++oi)
+    for (int i = 0; i < 10; ++i) {
+      const int w = outs[oi];
+      if (i == w || bytes[w] == 0 || bytes[i] == 0) continue;
+      if (overlap(ptrs[w], bytes[w], ptrs[i], bytes[i]))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s overlaps %s", w == 9 ? "row_stats" : views[w].name,
+                    i == 8 ? "lse" : (i == 9 ? "row_stats" : views[i].name));
+    }
+
+  const fastvr::BwdGrid g = fastvr::bwd_grid(B, H, Nq, Nkv, chunk_len);
+  if (g.q.n_items > fastvr::kMaxFwdItems || g.n_kv_items > fastvr::kMaxFwdItems)
+    return fail(FASTVR_ERR_UNSUPPORTED, "problem needs too many workgroups");
+
+  fastvr::BwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.dout = dout; a.o = o; a.lse = lse;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.row_stats = row_stats;
+  a.B = B; a.H = H; a.nq = Nq; a.nkv = Nkv; a.d = d;
+  a.chunk_len = chunk_len;
+  a.q_chunk_offset = q_chunk_offset;
+  a.window_chunks = window_chunks;
+  a.scale = scale;
+  const hipError_t e = fastvr::launch_chunk_attn_bwd(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "chunk_attn_bwd launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new, int64_t B,
                                      int64_t H, int64_t d, int64_t capacity, int64_t cache_len, int64_t n_new,
                                      void* stream) {

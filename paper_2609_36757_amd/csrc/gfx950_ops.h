@@ -73,6 +73,21 @@ static __device__ __forceinline__ void dma16(uint32_t lds_addr, uint32_t voff, i
                : "memory", "m0");
 }
 
+// The same with 4 bytes per lane (buffer_load_dword ... lds): lane data lands
+// at lds_addr + 4 * lane; only a 4-byte aligned source is needed.
+static __device__ __forceinline__ void dma4(uint32_t lds_addr, uint32_t voff, i32x4 rsrc, int soff) {
+  rsrc.x = __builtin_amdgcn_readfirstlane(rsrc.x);
+  rsrc.y = __builtin_amdgcn_readfirstlane(rsrc.y);
+  rsrc.z = __builtin_amdgcn_readfirstlane(rsrc.z);
+  rsrc.w = __builtin_amdgcn_readfirstlane(rsrc.w);
+  soff = __builtin_amdgcn_readfirstlane(soff);
+  lds_addr = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+               : "memory", "m0");
+}
+
 static __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
@@ -88,13 +103,10 @@ static __device__ __forceinline__ void barrier() {
 // s_waitcnt vmcnt(N): every DMA issued by this wave except the newest N
 // instructions has landed (inline assembly, so the compiler cannot relax it)
 template <int N>
-__device__ __forceinline__ void wait_vmcnt();
-template <>
-__device__ __forceinline__ void wait_vmcnt<0>() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-template <>
-__device__ __forceinline__ void wait_vmcnt<2>() { asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); }
-template <>
-__device__ __forceinline__ void wait_vmcnt<4>() { asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); }
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"i"(N) : "memory");
+}
 
 // instruction-group ordering hints for the scheduler (sched_group_barrier masks)
 #define SCHED_MFMA 0x008

@@ -49,6 +49,39 @@ constexpr int64_t kMaxTokenStride = int64_t(1) << 22;
 FwdGrid fwd_grid(int64_t B, int64_t H, int64_t nq, int64_t chunk_len);
 hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream);
 
+// Backward of one chunk-causal attention call.  All tensors are contiguous
+// [B, N, H, d] (lse and the row statistics [B, H, Nq]).
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;    // bf16 upstream gradient dL/dO
+  const float* o;      // forward output
+  const float* lse;    // forward natural-log LSE
+  float* dq;
+  float* dk;
+  float* dv;
+  float* row_stats;    // [B, H, Nq, 2] workspace: (lse * log2 e, rowsum(dO * O))
+  int64_t B, H, nq, nkv, d;
+  int64_t chunk_len, q_chunk_offset, window_chunks;
+  float scale;
+};
+
+struct BwdGrid {
+  FwdGrid q;               // dQ kernel: query tiles, as in the forward
+  int64_t n_kchunks;       // key chunks of the key range
+  int64_t kblocks_full;    // key blocks of a full chunk
+  int64_t kblocks_last;    // key blocks of the last (possibly ragged) chunk
+  int64_t n_kv_items;      // workgroups of the dK/dV kernel
+};
+
+constexpr int kBwdDqThreads = 512;   // 8 wave64, 32 queries each
+constexpr int kBwdDkvThreads = 256;  // 4 wave64, 32 keys each
+constexpr int kBwdKeysPerItem = 128;
+
+BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len);
+hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream);
+
 hipError_t launch_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
                             int64_t B, int64_t H, int64_t d, int64_t capacity, int64_t cache_len,
                             int64_t n_new, hipStream_t stream);

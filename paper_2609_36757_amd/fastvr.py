@@ -19,7 +19,7 @@ ERR_CAPACITY = 3
 ERR_HIP = 4
 
 EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
-            "fastvr_chunk_attn_ring_step", "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
+            "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
 
 _i64 = ctypes.c_int64
 _vp = ctypes.c_void_p
@@ -52,6 +52,9 @@ def load() -> ctypes.CDLL:
     lib.fastvr_chunk_attn_ring_step.restype = ctypes.c_int
     lib.fastvr_chunk_attn_ring_step.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64,
                                                 _i64, _i64, ctypes.c_float, _vp]
+    lib.fastvr_chunk_attn_bwd.restype = ctypes.c_int
+    lib.fastvr_chunk_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64,
+                                          _i64, _i64, _i64, _i64, ctypes.c_float, _vp]
     lib.fastvr_status_string.restype = ctypes.c_char_p
     lib.fastvr_status_string.argtypes = [ctypes.c_int]
     lib.fastvr_last_error.restype = ctypes.c_char_p
@@ -100,6 +103,12 @@ def ring_step_raw(q_new, k_new, v_new, k_ring, v_ring, o, lse, B, H, n_new, d, c
                   window_chunks, scale, stream=0) -> int:
     return load().fastvr_chunk_attn_ring_step(q_new, k_new, v_new, k_ring, v_ring, o, lse, B, H, n_new, d,
                                               chunk_len, chunk_index, window_chunks, scale, stream)
+
+
+def bwd_raw(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+            window_chunks, scale, stream=0) -> int:
+    return load().fastvr_chunk_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chunk_len,
+                                        q_chunk_offset, window_chunks, scale, stream)
 
 
 # ---------------------------------------------------------------------------
@@ -212,3 +221,40 @@ def chunk_attn_ring_step(q_new, k_new, v_new, k_ring, v_ring, *, chunk_len: int,
                          out.data_ptr(), lse.data_ptr() if lse is not None else None, B, H, n_new, d, chunk_len,
                          chunk_index, window_chunks, scale, _stream_handle(stream)))
     return out, lse
+
+
+def chunk_attn_bwd(q, k, v, o, lse, dout, *, chunk_len: int, q_chunk_offset: int = 0, window_chunks: int = -1,
+                   scale: float | None = None, dq=None, dk=None, dv=None, row_stats=None, stream=None):
+    """Gradients (dq, dk, dv), fp32, of chunk_attn for the upstream gradient ``dout``.
+
+    q/dout [B, Nq, H, d] and k/v [B, Nkv, H, d] bf16, o fp32 [B, Nq, H, d] and
+    lse fp32 [B, H, Nq] from the forward call with the same mask arguments and
+    scale; all contiguous.  ``row_stats`` (fp32 [B, H, Nq, 2]) is a workspace the
+    call fills with (LSE * log2 e, rowsum(dO * O))."""
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor")
+    B, Nq, H, d = q.shape
+    Nkv = k.shape[1]
+    if k.shape != (B, Nkv, H, d) or v.shape != k.shape or dout.shape != q.shape:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)} "
+                         f"dout {tuple(dout.shape)}")
+    for name, t, shape in (("o", o, (B, Nq, H, d)), ("lse", lse, (B, H, Nq))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 {list(shape)} tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    outs = []
+    for name, t, shape in (("dq", dq, (B, Nq, H, d)), ("dk", dk, (B, Nkv, H, d)), ("dv", dv, (B, Nkv, H, d)),
+                           ("row_stats", row_stats, (B, H, Nq, 2))):
+        if t is None:
+            t = torch.empty(shape, dtype=torch.float32, device=q.device)
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 {list(shape)} tensor")
+        outs.append(t)
+    dq, dk, dv, row_stats = outs
+    _check(bwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), dout.data_ptr(),
+                   dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), row_stats.data_ptr(), B, H, Nq, Nkv, d, chunk_len,
+                   q_chunk_offset, window_chunks, scale, _stream_handle(stream)))
+    return dq, dk, dv

@@ -14,7 +14,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 # Distinct fake addresses, 1 TiB apart, for calls that must fail validation:
 # every case below is rejected on the host before the HIP runtime is touched.
-Q, K, V, O, LSE, RK, RV = ((i + 1) << 40 for i in range(7))
+Q, K, V, O, LSE, RK, RV, DO, DQ, DK, DV, RS = ((i + 1) << 40 for i in range(12))
 BIG = 1 << 62
 
 
@@ -40,7 +40,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 2
+    assert lib.fastvr_abi_version() == 3
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -193,6 +193,54 @@ def test_ring_step_rejects(lib, kw, status, needle):
 @pytest.mark.parametrize("kw", [dict(B=0), dict(H=0)])
 def test_ring_step_empty_is_ok(lib, kw):
     assert _ring(**kw) == fastvr.OK
+
+
+BWD_GOOD = dict(q=Q, k=K, v=V, o=O, lse=LSE, dout=DO, dq=DQ, dk=DK, dv=DV, rs=RS, B=1, H=2, Nq=64, Nkv=64, d=64,
+                chunk_len=16, q_chunk_offset=0, window_chunks=-1, scale=0.125)
+
+
+def _bwd(**kw):
+    a = dict(BWD_GOOD)
+    a.update(kw)
+    return fastvr.bwd_raw(a["q"], a["k"], a["v"], a["o"], a["lse"], a["dout"], a["dq"], a["dk"], a["dv"], a["rs"],
+                          a["B"], a["H"], a["Nq"], a["Nkv"], a["d"], a["chunk_len"], a["q_chunk_offset"],
+                          a["window_chunks"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(q=None), fastvr.ERR_INVALID_ARGUMENT, "q is NULL"),
+    (dict(dout=None), fastvr.ERR_INVALID_ARGUMENT, "dout is NULL"),
+    (dict(o=None), fastvr.ERR_INVALID_ARGUMENT, "o is NULL"),
+    (dict(dq=None), fastvr.ERR_INVALID_ARGUMENT, "dq is NULL"),
+    (dict(dk=None), fastvr.ERR_INVALID_ARGUMENT, "dk is NULL"),
+    (dict(dv=None), fastvr.ERR_INVALID_ARGUMENT, "dv is NULL"),
+    (dict(lse=None), fastvr.ERR_INVALID_ARGUMENT, "lse or row_stats is NULL"),
+    (dict(rs=None), fastvr.ERR_INVALID_ARGUMENT, "lse or row_stats is NULL"),
+    (dict(dk=DK + 8), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (dict(rs=RS + 2), fastvr.ERR_INVALID_ARGUMENT, "4-byte aligned"),
+    (dict(B=-1), fastvr.ERR_INVALID_ARGUMENT, "negative size"),
+    (dict(d=96), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(chunk_len=0), fastvr.ERR_INVALID_ARGUMENT, "chunk_len"),
+    (dict(q_chunk_offset=-1), fastvr.ERR_INVALID_ARGUMENT, "q_chunk_offset"),
+    (dict(window_chunks=-2), fastvr.ERR_INVALID_ARGUMENT, "window_chunks"),
+    (dict(scale=float("nan")), fastvr.ERR_INVALID_ARGUMENT, "scale"),
+    (dict(Nkv=63), fastvr.ERR_INVALID_ARGUMENT, "would not see its own key"),
+    (dict(Nkv=0), fastvr.ERR_INVALID_ARGUMENT, "no keys"),
+    (dict(Nkv=1 << 31, Nq=64), fastvr.ERR_UNSUPPORTED, "2^31"),
+    (dict(H=1 << 16), fastvr.ERR_UNSUPPORTED, "H * d"),
+    (dict(dq=Q + 64), fastvr.ERR_INVALID_ARGUMENT, "dq overlaps q"),
+    (dict(dk=DV), fastvr.ERR_INVALID_ARGUMENT, "dk overlaps dv"),
+    (dict(rs=LSE), fastvr.ERR_INVALID_ARGUMENT, "row_stats overlaps lse"),
+    (dict(dv=K + 4096), fastvr.ERR_INVALID_ARGUMENT, "dv overlaps k"),
+])
+def test_bwd_rejects(lib, kw, status, needle):
+    assert _bwd(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(H=0), dict(Nq=0, Nkv=0)])
+def test_bwd_empty_is_ok(lib, kw):
+    assert _bwd(**kw) == fastvr.OK
 
 
 def test_error_is_thread_local(lib):

@@ -559,3 +559,78 @@ def test_bwd_pins_catch_a_dropped_row_term(monkeypatch):
     do = np.random.default_rng(6).standard_normal(q.shape)
     good = orig(q, k, v, do, chunk_len=5, window_chunks=1, scale=0.5)[0]
     assert np.abs(bad(q, k, v, do, chunk_len=5, window_chunks=1, scale=0.5)[0] - good).max() > 1e-3
+
+
+def _autograd_grads(q, k, v, do, L, off, W, scale):
+    """(dq, dk, dv) by torch autograd through an explicitly masked fp64 softmax."""
+    nq, nkv = q.shape[1], k.shape[1]
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (q, k, v))
+    mask = torch.tensor(oracle.visibility_mask(nq, nkv, L, off, W))
+    s = torch.einsum("bihd,bjhd->bhij", tq, tk) * scale
+    s = s.masked_fill(~mask, float("-inf"))
+    o = torch.einsum("bhij,bjhd->bihd", torch.softmax(s, dim=-1), tv)
+    (o * torch.tensor(do)).sum().backward()
+    return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
+
+
+@pytest.mark.parametrize("W,off,nq,nkv,L", [(-1, 0, 45, 45, 10), (1, 2, 21, 41, 7), (0, 0, 30, 30, 6)])
+def test_bwd_rows_subset_matches_autograd(W, off, nq, nkv, L):
+    """attention_bwd(rows=...) returns exactly those rows of dQ; given every
+    query of the last chunk it returns the full dK / dV of that chunk's keys
+    (no other query sees them)."""
+    B, H, d, scale = 1, 2, 8, 0.4
+    q, k, v = _rand(B, nq, nkv, H, d, seed=140 + nq)
+    do = np.random.default_rng(nq + 1).standard_normal((B, nq, H, d))
+    gq, gk, gv = _autograd_grads(q, k, v, do, L, off, W, scale)
+    rr = np.array([0, 3, nq // 2, nq - 1])
+    dq, _, _ = oracle.attention_bwd(q, k, v, do, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=scale,
+                                    rows=rr)
+    np.testing.assert_allclose(dq, gq[:, rr], rtol=0, atol=1e-11)
+    last_q = ((off * L + nq - 1) // L - off) * L        # first local row of the last query chunk
+    last_k = (off * L + nq - 1) // L * L                 # first key row of that chunk
+    _, dk, dv = oracle.attention_bwd(q, k, v, do, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=scale,
+                                     rows=np.arange(last_q, nq))
+    np.testing.assert_allclose(dk[:, last_k:off * L + nq], gk[:, last_k:off * L + nq], rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv[:, last_k:off * L + nq], gv[:, last_k:off * L + nq], rtol=0, atol=1e-11)
+
+
+@pytest.mark.parametrize("W,off,nq,nkv,L", [(-1, 0, 40, 40, 8), (1, 0, 37, 37, 6), (2, 3, 10, 30, 5),
+                                            (0, 0, 33, 33, 7), (1, 4, 12, 40, 8)])
+def test_bwd_keys_matches_autograd(W, off, nq, nkv, L):
+    """attention_bwd_keys, fed the oracle's own LSE and D, gives autograd's dK /
+    dV for every key, including keys no query sees (zero); rows that see none
+    of the requested keys are never read (NaN there changes nothing)."""
+    B, H, d, scale = 2, 2, 8, 0.35
+    q, k, v = _rand(B, nq, nkv, H, d, seed=150 + nq)
+    do = np.random.default_rng(nq + 2).standard_normal((B, nq, H, d))
+    gq, gk, gv = _autograd_grads(q, k, v, do, L, off, W, scale)
+    o, lse = oracle.attention(q, k, v, chunk_len=L, q_chunk_offset=off, window_chunks=W, scale=scale)
+    delta = oracle.attention_bwd_delta(o, do)
+    keys = np.arange(nkv)
+    dk, dv = oracle.attention_bwd_keys(q, k, v, do, keys, lse, delta, chunk_len=L, q_chunk_offset=off,
+                                       window_chunks=W, scale=scale)
+    np.testing.assert_allclose(dk, gk, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv, gv, rtol=0, atol=1e-11)
+    # keys of the last key chunk only: poison the statistics of rows that do not see them
+    kc = (nkv - 1) // L
+    sel = np.arange(kc * L, nkv)
+    seen = oracle.visibility_mask(nq, nkv, L, off, W)[:, sel].any(axis=1)
+    lse_p, delta_p = lse.copy(), delta.copy()
+    lse_p[:, :, ~seen] = np.nan
+    delta_p[:, :, ~seen] = np.nan
+    dk2, dv2 = oracle.attention_bwd_keys(q, k, v, do, sel, lse_p, delta_p, chunk_len=L, q_chunk_offset=off,
+                                         window_chunks=W, scale=scale)
+    np.testing.assert_allclose(dk2, gk[:, sel], rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv2, gv[:, sel], rtol=0, atol=1e-11)
+
+
+def test_bwd_keys_pin_catches_a_wrong_window(monkeypatch):
+    """attention_bwd_keys with the window check dropped fails the autograd pin."""
+    q, k, v = _rand(1, 30, 30, 1, 4, seed=160)
+    do = np.random.default_rng(7).standard_normal(q.shape)
+    gq, gk, gv = _autograd_grads(q, k, v, do, 6, 0, 1, 0.5)
+    o, lse = oracle.attention(q, k, v, chunk_len=6, window_chunks=1, scale=0.5)
+    delta = oracle.attention_bwd_delta(o, do)
+    dk, dv = oracle.attention_bwd_keys(q, k, v, do, np.arange(30), lse, delta, chunk_len=6, window_chunks=-1,
+                                       scale=0.5)
+    assert np.abs(dv - gv).max() > 1e-3
