@@ -106,7 +106,7 @@ def backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, reps: int):
     o, lse = fastvr.chunk_attn(qd, kd, vd, chunk_len=w.chunk_len, window_chunks=w.window_chunks, scale=w.scale)
     dq = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
     dk, dv = torch.empty_like(dq), torch.empty_like(dq)
-    rs = torch.empty((w.B, w.H, w.n_tokens, 2), dtype=torch.float32, device=dev)
+    rs = torch.empty((w.B, w.H, 2, w.n_tokens), dtype=torch.float32, device=dev)
     ms = _time_ms(torch, cur, lambda: fastvr.chunk_attn_bwd(qd, kd, vd, o, lse, dout, chunk_len=w.chunk_len,
                                                             window_chunks=w.window_chunks, scale=w.scale, dq=dq,
                                                             dk=dk, dv=dv, row_stats=rs), reps)

@@ -162,8 +162,9 @@ fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, 
  *   dq          fp32 [B, Nq,  H, d] contiguous   output, fully overwritten
  *   dk, dv      fp32 [B, Nkv, H, d] contiguous   outputs, fully overwritten (zero for
  *                                                keys no query sees)
- *   row_stats   fp32 [B, H, Nq, 2]  contiguous   caller-owned workspace, written by
- *                                                the call: (LSE_i * log2 e, D_i)
+ *   row_stats   fp32 [B, H, 2, Nq]  contiguous   caller-owned workspace, written by
+ *                                                the call: plane 0 LSE_i * log2 e,
+ *                                                plane 1 -D_i
  * Mask arguments (chunk_len, q_chunk_offset, window_chunks) and scale are those
  * of the forward call that produced o and lse.  Two kernels run in order on
  * `stream`; sums run in a fixed order, so results are reproducible bit for bit.

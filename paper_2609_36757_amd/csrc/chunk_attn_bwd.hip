@@ -13,16 +13,16 @@
 // Two kernels, no atomics, so every gradient is a fixed-order sum (results are
 // reproducible bit for bit):
 //  * dQ kernel (query-stationary, the forward's grid): 8 waves, 32 queries each,
-//    Q and dO fragments in registers.  It first writes (LSE * log2 e, D) of its
+//    Q and dO fragments in registers.  It first writes LSE * log2 e and -D of its
 //    rows to a workspace, then per 64-key tile computes S^T = K Q^T and
 //    dP^T = V dO^T (one query per lane, 16 keys per lane), P^T and dS^T in
 //    registers, and dQ^T += K^T dS^T.
 //  * dK/dV kernel (key-stationary): a workgroup owns 128 keys of one chunk
-//    (4 waves, 32 keys each, K and V fragments in registers) and walks the
-//    64-query tiles of the queries that see that chunk: S = Q K^T and
-//    dP = dO V^T (one key per lane, 16 queries per lane), then
-//    dV^T += dO^T P and dK^T += Q^T dS.  Both accumulators stay in registers
-//    (one wave per SIMD).
+//    and walks the 64-query tiles of the queries that see that chunk.  Each
+//    32 keys belong to a wave pair: one wave holds K, computes S = Q K^T (one
+//    key per lane, 16 queries per lane), P, and dV^T += dO^T P; the other holds
+//    V, computes dP = dO V^T and dS = P (dP - D) from the first wave's P, and
+//    dK^T += Q^T dS.
 // All products are v_mfma_f32_32x32x16_bf16 with fp32 accumulation; P and dS
 // are rounded to bf16 as MFMA operands.
 //
@@ -45,13 +45,17 @@ namespace {
 
 using namespace dev;
 
+#ifndef FASTVR_PRIO
+#define FASTVR_PRIO 1  // raise the wave priority during matrix-core slots
+#endif
+
 constexpr int kTile = 64;  // rows per staged tile: keys (dQ) or queries (dK/dV)
 constexpr int kStages = 3;
 constexpr int kDqWaves = kBwdDqThreads / 64;    // 8
-constexpr int kDkvWaves = kBwdDkvThreads / 64;  // 4
+constexpr int kDkvWaves = kBwdDkvThreads / 64;  // 8 (two groups of 4)
 constexpr int kDqRows = 32 * kDqWaves;          // 256 queries per dQ workgroup
 static_assert(kDqRows == kFwdRowsPerItem, "the dQ grid is the forward's");
-static_assert(32 * kDkvWaves == kBwdKeysPerItem, "32 keys per dK/dV wave");
+static_assert(32 * (kDkvWaves / 2) == kBwdKeysPerItem, "32 keys per dK/dV wave pair");
 
 struct BwdParams {
   const uint16_t* q;
@@ -63,7 +67,7 @@ struct BwdParams {
   float* dq;
   float* dk;
   float* dv;
-  float* rs;             // row statistics [B, H, nq, 2]
+  float* rs;             // row statistics [B, H, 2, nq]: LSE log2 e, then -D
   int64_t q_sb, kv_sb;   // batch strides (elements) of the query-side and key-side tensors
   int32_t st;            // token stride H * d (elements), all tensors
   int32_t nq, nkv, chunk_len, q_chunk_offset, window;  // window -1 = unbounded
@@ -280,9 +284,9 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
     lse2 = row_ok ? lse * 1.44269504088896340736f : 0.f;
     dlt = row_ok ? dlt : 0.f;
     if (row_ok && hh == 0) {
-      float* rs = p.rs + (((int64_t)b * p.H + h) * p.nq + row) * 2;
+      float* rs = p.rs + ((int64_t)b * p.H + h) * 2 * p.nq + row;
       rs[0] = lse2;
-      rs[1] = dlt;
+      rs[p.nq] = -dlt;
     }
   }
   f32x16 acc[D / 32];
@@ -358,19 +362,156 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
 }
 
 // -------------------------------------------------------------- dK/dV kernel
+//
+// Eight waves in two groups that share the four SIMDs one-to-one.  Wave pair
+// (a, a + 4) owns 32 keys: group A (waves 0-3) computes S = Q K^T, P and
+// dV^T += dO^T P; group B (waves 4-7) computes dP - D = dO V^T - D, dS = P (dP - D)
+// and dK^T += Q^T dS, taking P from group A through LDS as bf16 fragments.
+// Time is cut into slots separated by workgroup barriers, and the two groups
+// swap between a matrix-core slot and a vector-ALU slot every slot:
+//   slot 2t:   A  S(t) and dV += dO^T(t-1) P(t-1)       B  dS(t-1); DMA of Q(t+2), row stats(t+2)
+//   slot 2t+1: A  P(t) (exp2), P(t) to LDS; DMA dO(t+2)  B  dP(t) - D and dK += Q^T(t-1) dS(t-1)
+// A tile is read from slot 2t to slot 2t+3, so the LDS holds four stages.
+// The dP accumulator starts from -D (read from the row statistics), so
+// dP - D comes out of the MFMAs.
+
+constexpr int kDkvStages = 4;
 
 template <int D>
-__global__ __launch_bounds__(kBwdDkvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void
-chunk_attn_bwd_dkv_kernel(const BwdParams p) {
-  using Dma = TileDma<D, kDkvWaves>;
-  constexpr int kStage = Dma::kElems;
-  constexpr int kRsFloats = 2 * kTile;  // (LSE log2 e, D) of the tile's 64 queries
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kStages * kStage];
-  __shared__ __attribute__((aligned(16))) float rss[kStages * kRsFloats];
-  uint16_t* qs = smem;
-  uint16_t* dos = smem + kStages * kStage;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n = lane & 31, hh = lane >> 5;
+struct Dkv {
+  using Dma = TileDma<D, kDkvWaves / 2>;  // one group issues each operand
+  static constexpr int kStage = Dma::kElems;
+  static constexpr int kRs = 2 * kTile;  // floats per row-statistics stage: LSE log2 e, then -D
+  int lane, wave, pair, n, hh;
+  float c;
+  uint16_t* qs;
+  uint16_t* dos;
+  float* rss;
+  u32x4* pex;  // P exchange of this pair: [4 fragments][64 lanes]
+  TileReads<D> rd;
+  u32x4 kvf[D / 16];  // A: K fragments (B operand K^T); B: V fragments (V^T)
+  f32x16 acc[D / 32]; // A: dV^T; B: dK^T
+  f32x16 sp[2];       // A: S, then P; B: dP - D
+  u32x4 frag[4];      // A: bf16 P; B: bf16 dS
+
+  __device__ __forceinline__ const char* q_stage(int t) const {
+    return reinterpret_cast<const char*>(qs + (t & (kDkvStages - 1)) * kStage);
+  }
+  __device__ __forceinline__ const char* do_stage(int t) const {
+    return reinterpret_cast<const char*>(dos + (t & (kDkvStages - 1)) * kStage);
+  }
+  __device__ __forceinline__ const float* rs_stage(int t) const { return rss + (t & (kDkvStages - 1)) * kRs; }
+
+  // Group A, matrix-core slot: S(t) = Q K^T (when S_T) and dV^T += dO^T(t-1) P(t-1) (when PV)
+  template <bool S_T, bool PV>
+  __device__ __forceinline__ void a_mfma(int t) {
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
+    if (S_T) {
+      const char* qst = q_stage(t);
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(qst, mb, kk), kvf[kk], kk == 0 ? f32x16{} : sp[mb]);
+    }
+    if (PV) {
+      const char* dost = do_stage(t - 1);
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(dost, g, dm), frag[g], acc[dm]);
+    }
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
+  }
+  // Group A, vector-ALU slot: P(t) = exp2(S c - LSE log2 e) for query rows
+  // 32 mb + 8 g + 4 hh + r, rounded to bf16 fragments, and handed to group B.
+  // Rows past the query range have Q = 0 and zero statistics, so P = 1 there,
+  // and dO = 0 and -D = 0 make their dV and dS terms vanish.
+  __device__ __forceinline__ void a_valu(int t) {
+    const float* l2 = rs_stage(t);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(l2 + 32 * mb + 8 * g + 4 * hh);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          sp[mb][4 * g + r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[mb][4 * g + r], c, -l4[r]));
+      }
+    pack_bf16(sp, frag);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) pex[g * 64 + lane] = frag[g];
+  }
+  // Group B, matrix-core slot: dP(t) - D = dO V^T - D (when DP) and dK^T +=
+  // Q^T(t-1) dS(t-1) (when DK)
+  template <bool DP, bool DK>
+  __device__ __forceinline__ void b_mfma(int t) {
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
+    if (DP) {
+      const char* dost = do_stage(t);
+      const float* nd = rs_stage(t) + kTile;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(nd + 32 * mb + 8 * g + 4 * hh);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sp[mb][4 * g + r] = d4[r];
+        }
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(dost, mb, kk), kvf[kk], sp[mb]);
+    }
+    if (DK) {
+      const char* qst = q_stage(t - 1);
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(qst, g, dm), frag[g], acc[dm]);
+    }
+#if FASTVR_PRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
+  }
+  // Group B, vector-ALU slot: dS(t) = P(t) (dP - D), rounded to bf16 fragments
+  __device__ __forceinline__ void b_valu() {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const bf16x8 p8 = __builtin_bit_cast(bf16x8, pex[g * 64 + lane]);
+#pragma unroll
+      for (int r = 0; r < 8; ++r) sp[g >> 1][8 * (g & 1) + r] *= (float)p8[r];
+    }
+    pack_bf16(sp, frag);
+  }
+};
+
+template <int D>
+__global__ __launch_bounds__(kBwdDkvThreads) void chunk_attn_bwd_dkv_kernel(const BwdParams p) {
+  using K = Dkv<D>;
+  using Dma = typename K::Dma;
+  constexpr int kStage = K::kStage;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kDkvStages * kStage];
+  __shared__ __attribute__((aligned(16))) float rss[kDkvStages * K::kRs];
+  __shared__ __attribute__((aligned(16))) u32x4 pex[(kDkvWaves / 2) * 4 * 64];
+  K a;
+  a.qs = smem;
+  a.dos = smem + kDkvStages * kStage;
+  a.rss = rss;
+  const int tid = threadIdx.x;
+  a.lane = tid & 63;
+  a.wave = tid >> 6;
+  a.pair = a.wave & 3;
+  const int group = a.wave >> 2;  // 0: A (S, P, dV), 1: B (dP, dS, dK)
+  a.n = a.lane & 31;
+  a.hh = a.lane >> 5;
+  a.c = p.c;
+  a.pex = pex + a.pair * 4 * 64;
 
   // item -> (key chunk, batch*head, key block), first chunk first: with an
   // unbounded window the earliest keys are seen by the most queries
@@ -395,8 +536,8 @@ chunk_attn_bwd_dkv_kernel(const BwdParams p) {
   const int b = bh / p.H, h = bh - (bh / p.H) * p.H;
   const int L = p.chunk_len;
   const int key_end = (L < p.nkv - ck * L) ? (ck + 1) * L : p.nkv;
-  const int key0 = ck * L + kblk * kBwdKeysPerItem + wave * 32;  // this wave's first key
-  const int key = key0 + n;
+  const int key0 = ck * L + kblk * kBwdKeysPerItem + a.pair * 32;  // this pair's first key
+  const int key = key0 + a.n;
   // queries that see key chunk ck: local chunks [ck - q_off, ck + W - q_off]
   int cl_lo = ck - p.q_chunk_offset;
   if (cl_lo < 0) cl_lo = 0;
@@ -409,136 +550,114 @@ chunk_attn_bwd_dkv_kernel(const BwdParams p) {
   const int st = p.st;
   const uint16_t* qb = p.q + (int64_t)b * p.q_sb + (int64_t)h * D;
   const uint16_t* dob = p.dout + (int64_t)b * p.q_sb + (int64_t)h * D;
-  const float* rsb = p.rs + ((int64_t)b * p.H + h) * p.nq * 2;
+  const float* rsb = p.rs + ((int64_t)b * p.H + h) * 2 * p.nq;  // planes: LSE log2 e, -D
 
   Dma dma;
-  dma.init(wave, lane, st);
-  TileReads<D> rd;
-  rd.init(lane);
-  auto tile_rows = [&](int j) { return qhi - (qlo + j * kTile); };
-  // row statistics of tile j: 64 pairs = 128 floats, 4 bytes per lane from the
-  // first 32 lanes of each wave (exec-masked; the tile may start at an odd
-  // row, so 16-byte units could be misaligned), zero past the query range
-  auto load_rs = [&](int j, int stage) {
-    if (lane < 32) {
-      const int rows = tile_rows(j);
-      const i32x4 rsrc = make_vsharp(rsb + (int64_t)(qlo + j * kTile) * 2, rows > 0 ? (int64_t)rows * 8 : 0);
-      const uint32_t la = lds_addr(rss + stage * kRsFloats) + (uint32_t)(wave * 32 * 4);
-      dma4(la, (uint32_t)((wave * 32 + lane) * 4), rsrc, 0);
+  dma.init(a.pair, a.lane, st);
+  a.rd.init(a.lane);
+  auto tile_rows = [&](int t) { return qhi - (qlo + t * kTile); };
+  // Group B: Q tile t and its row statistics (wave pair w: plane w >> 1, rows
+  // 32 (w & 1) .. + 31, 4 bytes per lane from 32 exec-masked lanes; the tile
+  // may start at an odd row)
+  auto load_b = [&](int t) {
+    dma.load(qb + (int64_t)(qlo + t * kTile) * st, tile_rows(t), st, a.qs + (t & (kDkvStages - 1)) * kStage, a.pair);
+    if (a.lane < 32) {
+      const int r0 = 32 * (a.pair & 1);
+      int rows = tile_rows(t) - r0;
+      rows = rows < 0 ? 0 : (rows > 32 ? 32 : rows);
+      const float* src = rsb + (int64_t)(a.pair >> 1) * p.nq + qlo + t * kTile + r0;
+      const i32x4 rsrc = make_vsharp(src, (int64_t)rows * 4);
+      const uint32_t la = lds_addr(rss + (t & (kDkvStages - 1)) * K::kRs) + (uint32_t)(a.pair * 32 * 4);
+      dma4(la, (uint32_t)(a.lane * 4), rsrc, 0);
     }
   };
-  auto load_tile = [&](int j, int stage) {
-    dma.load(qb + (int64_t)(qlo + j * kTile) * st, tile_rows(j), st, qs + stage * kStage, wave);
-    dma.load(dob + (int64_t)(qlo + j * kTile) * st, tile_rows(j), st, dos + stage * kStage, wave);
-    load_rs(j, stage);
+  // Group A: dO tile t
+  auto load_a = [&](int t) {
+    dma.load(dob + (int64_t)(qlo + t * kTile) * st, tile_rows(t), st, a.dos + (t & (kDkvStages - 1)) * kStage,
+             a.pair);
   };
   if (n_tiles > 0) {
-    load_tile(0, 0);
-    load_tile(1, 1);
+    if (group == 0) {
+      load_a(0);
+      load_a(1);
+    } else {
+      load_b(0);
+      load_b(1);
+    }
   }
-
-  // K and V fragments (B operands K^T, V^T) of this wave's 32 keys
-  u32x4 kf[D / 16], vf[D / 16];
+  // K (group A) or V (group B) fragments of this pair's 32 keys
   {
     const int rows = key_end - key0;
     const int64_t koff = (int64_t)b * p.kv_sb + (int64_t)key0 * st + (int64_t)h * D;
-    const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k + koff, rows > 0 ? (int64_t)rows * st * 2 : 0);
-    const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v + koff, rows > 0 ? (int64_t)rows * st * 2 : 0);
+    const __amdgpu_buffer_rsrc_t rkv =
+        make_rsrc((group == 0 ? p.k : p.v) + koff, rows > 0 ? (int64_t)rows * st * 2 : 0);
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
-      const uint32_t e = (uint32_t)(n * st + kk * 16 + hh * 8);
-      kf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, e * 2u, 0, 0));
-      vf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, e * 2u, 0, 0));
+      const uint32_t e = (uint32_t)(a.n * st + kk * 16 + a.hh * 8);
+      a.kvf[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rkv, e * 2u, 0, 0));
     }
   }
-  f32x16 dka[D / 32], dva[D / 32];
 #pragma unroll
-  for (int dm = 0; dm < D / 32; ++dm) {
-    dka[dm] = f32x16{};
-    dva[dm] = f32x16{};
-  }
+  for (int dm = 0; dm < D / 32; ++dm) a.acc[dm] = f32x16{};
   wait_vmcnt<0>();
   __builtin_amdgcn_s_waitcnt(0x0F70);
   barrier();
 
-  const float c = p.c;
-  int s_cur = 0, s_next = 1, s_free = 2;
-  for (int j = 0; j < n_tiles; ++j) {
-    load_tile(j + 2, s_free);
-    const char* qst = reinterpret_cast<const char*>(qs + s_cur * kStage);
-    const char* dost = reinterpret_cast<const char*>(dos + s_cur * kStage);
-    const float* rst = rss + s_cur * kRsFloats;
-    f32x16 s[2], dp[2];
-    // S = Q K^T and dP = dO V^T: lane = key n, 16 queries per lane
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) s[mb] = mfma32(rd.row(qst, mb, kk), kf[kk], kk == 0 ? f32x16{} : s[mb]);
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) dp[mb] = mfma32(rd.row(dost, mb, kk), vf[kk], kk == 0 ? f32x16{} : dp[mb]);
-    // P = exp2(S c - LSE log2 e), dS = P (dP - D) per query row
-    // 32 mb + 8 g + 4 hh + r; rows past the query range have Q = dO = 0 and
-    // zero statistics, so P = 1 and dS = 0 there and they add nothing
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4* rp = reinterpret_cast<const f32x4*>(rst + 2 * (32 * mb + 8 * g + 4 * hh));
-        const f32x4 r01 = rp[0], r23 = rp[1];  // (lse2, D) of rows +0, +1 and +2, +3
-        const float l2[4] = {r01.x, r01.z, r23.x, r23.z};
-        const float dd[4] = {r01.y, r01.w, r23.y, r23.w};
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int v = 4 * g + r;
-          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][v], c, -l2[r]));
-          s[mb][v] = pv;
-          dp[mb][v] = pv * (dp[mb][v] - dd[r]);
-        }
-      }
-    u32x4 pf[4], dsf[4];
-    pack_bf16(s, pf);
-    pack_bf16(dp, dsf);
-    // dV^T += dO^T P and dK^T += Q^T dS
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int dm = 0; dm < D / 32; ++dm) dva[dm] = mfma32(rd.tr(dost, g, dm), pf[g], dva[dm]);
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int dm = 0; dm < D / 32; ++dm) dka[dm] = mfma32(rd.tr(qst, g, dm), dsf[g], dka[dm]);
-    wait_vmcnt<2 * Dma::kPer + 1>();
+  const int n = n_tiles;
+  for (int t = 0; t < n; ++t) {
+    // ---- slot 2t ----
+    if (group == 0) {
+      if (t == 0)
+        a.template a_mfma<true, false>(t);
+      else
+        a.template a_mfma<true, true>(t);
+    } else {
+      load_b(t + 2);
+      if (t > 0) a.b_valu();
+    }
     barrier();
-    const int s_old = s_cur;
-    s_cur = s_next;
-    s_next = s_free;
-    s_free = s_old;
+    // ---- slot 2t+1 ----
+    if (group == 0) {
+      a.a_valu(t);
+      load_a(t + 2);
+      wait_vmcnt<Dma::kPer>();
+    } else {
+      if (t == 0)
+        a.template b_mfma<true, false>(t);
+      else
+        a.template b_mfma<true, true>(t);
+      wait_vmcnt<Dma::kPer + 1>();
+    }
+    barrier();
+  }
+  if (n > 0) {
+    // ---- slot 2n: dV(n-1), dS(n-1) ----
+    if (group == 0)
+      a.template a_mfma<false, true>(n);
+    else
+      a.b_valu();
+    barrier();
+    // ---- slot 2n+1: dK(n-1) ----
+    if (group == 1) a.template b_mfma<false, true>(n);
   }
   wait_vmcnt<0>();
 
-  // dK = scale * dK^T, dV = dV^T: lane n holds dims dm * 32 + 8 g + 4 hh + 0..3 of key n
+  // dV = dV^T (group A), dK = scale * dK^T (group B): lane n holds dims
+  // dm * 32 + 8 g + 4 hh + 0..3 of key n
   if (key < key_end) {
     const int64_t off = (int64_t)b * p.kv_sb + (int64_t)key * st + (int64_t)h * D;
-    float* dko = p.dk + off;
-    float* dvo = p.dv + off;
-    const float sc = p.scale;
+    float* out = (group == 0 ? p.dv : p.dk) + off;
+    const float sc = group == 0 ? 1.0f : p.scale;
 #pragma unroll
     for (int dm = 0; dm < D / 32; ++dm)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        f32x4 kv, vv;
-        kv.x = dka[dm][4 * g + 0] * sc;
-        kv.y = dka[dm][4 * g + 1] * sc;
-        kv.z = dka[dm][4 * g + 2] * sc;
-        kv.w = dka[dm][4 * g + 3] * sc;
-        vv.x = dva[dm][4 * g + 0];
-        vv.y = dva[dm][4 * g + 1];
-        vv.z = dva[dm][4 * g + 2];
-        vv.w = dva[dm][4 * g + 3];
-        *reinterpret_cast<f32x4*>(dko + dm * 32 + g * 8 + hh * 4) = kv;
-        *reinterpret_cast<f32x4*>(dvo + dm * 32 + g * 8 + hh * 4) = vv;
+        f32x4 val;
+        val.x = a.acc[dm][4 * g + 0] * sc;
+        val.y = a.acc[dm][4 * g + 1] * sc;
+        val.z = a.acc[dm][4 * g + 2] * sc;
+        val.w = a.acc[dm][4 * g + 3] * sc;
+        *reinterpret_cast<f32x4*>(out + dm * 32 + g * 8 + a.hh * 4) = val;
       }
   }
 }

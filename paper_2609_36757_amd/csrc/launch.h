@@ -61,7 +61,7 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
-  float* row_stats;    // [B, H, Nq, 2] workspace: (lse * log2 e, rowsum(dO * O))
+  float* row_stats;    // [B, H, 2, Nq] workspace: lse * log2 e, then -rowsum(dO * O)
   int64_t B, H, nq, nkv, d;
   int64_t chunk_len, q_chunk_offset, window_chunks;
   float scale;
@@ -76,7 +76,7 @@ struct BwdGrid {
 };
 
 constexpr int kBwdDqThreads = 512;   // 8 wave64, 32 queries each
-constexpr int kBwdDkvThreads = 256;  // 4 wave64, 32 keys each
+constexpr int kBwdDkvThreads = 512;  // 8 wave64: 4 pairs, 32 keys each
 constexpr int kBwdKeysPerItem = 128;
 
 BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len);

@@ -229,8 +229,8 @@ def chunk_attn_bwd(q, k, v, o, lse, dout, *, chunk_len: int, q_chunk_offset: int
 
     q/dout [B, Nq, H, d] and k/v [B, Nkv, H, d] bf16, o fp32 [B, Nq, H, d] and
     lse fp32 [B, H, Nq] from the forward call with the same mask arguments and
-    scale; all contiguous.  ``row_stats`` (fp32 [B, H, Nq, 2]) is a workspace the
-    call fills with (LSE * log2 e, rowsum(dO * O))."""
+    scale; all contiguous.  ``row_stats`` (fp32 [B, H, 2, Nq]) is a workspace the
+    call fills with LSE * log2 e (plane 0) and -rowsum(dO * O) (plane 1)."""
     import torch
     for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
         if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
@@ -247,7 +247,7 @@ def chunk_attn_bwd(q, k, v, o, lse, dout, *, chunk_len: int, q_chunk_offset: int
         scale = 1.0 / math.sqrt(d)
     outs = []
     for name, t, shape in (("dq", dq, (B, Nq, H, d)), ("dk", dk, (B, Nkv, H, d)), ("dv", dv, (B, Nkv, H, d)),
-                           ("row_stats", row_stats, (B, H, Nq, 2))):
+                           ("row_stats", row_stats, (B, H, 2, Nq))):
         if t is None:
             t = torch.empty(shape, dtype=torch.float32, device=q.device)
         if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():

@@ -6,7 +6,8 @@ MFMAs with fp32 accumulation; besides the bf16 inputs (shared with the
 oracle) the only roundings of any size are P (operand of dV = P^T dO) and dS
 (operand of dQ = scale dS K and dK = scale dS^T Q) to bf16, each a relative
 error of at most u = 2^-8 per term.  A gradient element that sums terms t_m
-therefore carries an error of standard deviation at most u * sigma with
+therefore carries an error of standard deviation at most u * sigma (dK:
+sqrt(2) u sigma, since its dS is formed from the bf16-rounded P) with
 sigma = sqrt(sum_m t_m^2):
     sigma_dV[j, c] = sqrt(sum_i P_ij^2 dO_ic^2)
     sigma_dQ[i, c] = |scale| sqrt(sum_j dS_ij^2 k_jc^2)
@@ -126,21 +127,22 @@ def test_bwd_matches_oracle(dev, case):
 
 
 def test_bwd_row_stats_and_determinism(dev):
-    """The workspace holds (LSE log2 e, rowsum(dO * O)) per row, and a second
-    call reproduces every output bit for bit (fixed summation order)."""
+    """The workspace holds LSE log2 e and -rowsum(dO * O) per row (two planes),
+    and a second call reproduces every output bit for bit (fixed summation
+    order)."""
     B, H, d, N, L, W, seed = 2, 3, 128, 700, 160, 1, 31
     _announce(f"bwd row stats / determinism B={B} H={H} d={d} N={N} L={L} W={W}")
     q, k, v = make_qkv(B, N, N, H, d, seed)
     do = _draw_do(B, N, H, d, seed + 1)
     (qd, kd, vd, dod, o, lse), (dq, dk, dv) = _gpu_fwd_bwd(dev, q, k, v, do, L, 0, W, default_scale(d))
-    rs = torch.empty((B, H, N, 2), dtype=torch.float32, device=dev)
+    rs = torch.empty((B, H, 2, N), dtype=torch.float32, device=dev)
     dq2, dk2, dv2 = fastvr.chunk_attn_bwd(qd, kd, vd, o, lse, dod, chunk_len=L, window_chunks=W, row_stats=rs)
     torch.cuda.synchronize()
     assert torch.equal(dq, dq2) and torch.equal(dk, dk2) and torch.equal(dv, dv2)
     lse2 = (lse * np.float32(LOG2E)).cpu().numpy()
-    np.testing.assert_allclose(rs[..., 0].cpu().numpy(), lse2, rtol=2e-7, atol=1e-6)
+    np.testing.assert_allclose(rs[:, :, 0].cpu().numpy(), lse2, rtol=2e-7, atol=1e-6)
     dref = oracle.attention_bwd_delta(to_np(o), do)
-    np.testing.assert_allclose(rs[..., 1].cpu().numpy(), dref, rtol=1e-5, atol=1e-5)
+    np.testing.assert_allclose(-rs[:, :, 1].cpu().numpy(), dref, rtol=1e-5, atol=1e-5)
 
 
 def test_bwd_no_queries_zeroes_key_gradients(dev):
