@@ -18,3 +18,4 @@ from .chunk_attention import (  # noqa: F401
     softmax_weights,
     visibility_mask,
 )
+from .one_step import one_step_update, target_velocity  # noqa: F401

@@ -634,3 +634,45 @@ def test_bwd_keys_pin_catches_a_wrong_window(monkeypatch):
     dk, dv = oracle.attention_bwd_keys(q, k, v, do, np.arange(30), lse, delta, chunk_len=6, window_chunks=-1,
                                        scale=0.5)
     assert np.abs(dv - gv).max() > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# one-step latent update (Sec. 3.2, Eq. 9)
+# ---------------------------------------------------------------------------
+
+def test_one_step_hand_example():
+    """The worked example of tests/golden/one_step_example.csv (sigma = 0.75)."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "one_step_example.csv")
+    rows = np.array([[float(x) for x in line.split(",")] for line in open(path)
+                     if line.strip() and not line.startswith("#") and not line.startswith("z_lq")])
+    np.testing.assert_array_equal(oracle.one_step_update(rows[:, 0], rows[:, 1], 0.75), rows[:, 2])
+
+
+def test_one_step_recovers_hq_endpoint_from_target_velocity():
+    """With the target velocity of Eq. 4 (the linear trajectory of Eq. 3), the
+    update of Eq. 9 returns the HQ endpoint."""
+    rng = np.random.default_rng(200)
+    z_lq, z_hq = rng.standard_normal((2, 3, 5, 7))
+    for sigma in (0.3, 0.8, 1.0):
+        u = oracle.target_velocity(z_lq, z_hq, sigma)
+        np.testing.assert_allclose(oracle.one_step_update(z_lq, u, sigma), z_hq, rtol=0, atol=1e-14)
+
+
+def test_one_step_closed_forms_and_shape_check():
+    rng = np.random.default_rng(201)
+    z, v = rng.standard_normal((2, 64))
+    np.testing.assert_array_equal(oracle.one_step_update(z, v, 0.0), z)          # sigma = 0: no move
+    np.testing.assert_array_equal(oracle.one_step_update(z, np.zeros(64), 0.9), z)
+    np.testing.assert_array_equal(oracle.one_step_update(np.zeros(64), v, 1.0), -v)
+    with pytest.raises(ValueError):
+        oracle.one_step_update(z, v[:10], 0.5)
+
+
+def test_one_step_pin_catches_a_sign_error(monkeypatch):
+    """An update with the sign of sigma flipped fails the endpoint pin."""
+    import oracle.one_step as os_mod
+    rng = np.random.default_rng(202)
+    z_lq, z_hq = rng.standard_normal((2, 16))
+    u = oracle.target_velocity(z_lq, z_hq, 0.5)
+    bad = os_mod._f64(z_lq) + 0.5 * u
+    assert np.abs(bad - z_hq).max() > 1e-3
