@@ -11,8 +11,8 @@ value = effective (unmasked) TFLOP/s of the whole step: 4 * d * visible pairs
 
 After the timed steps (and outside them) it reports ms/call and TFLOP/s of
 the 480p-shaped and wide sliding-window calls, of the W = 1 ring-cache
-streaming step and of the backward of the 1080p call (``other_workloads``),
-then the fp64 oracle baseline.
+streaming step, of the backward of the 1080p call and of the one-step latent
+update (``other_workloads``), then the fp64 oracle baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
 """
@@ -118,6 +118,28 @@ def backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, reps: int):
                     "recomputed by both)"}
 
 
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def one_step_update_timing(torch, fastvr, dev, cur):
+    """The one-step latent update z_hat = z_LQ - sigma v (fp32 out) on the latent of
+    the 1080p sequence (48 channels x 8 latent frames x 68 x 120) and on a
+    2^28-element latent, as algorithmic HBM bytes (2 + 2 + 4 per element) per
+    second against the 8 TB/s peak."""
+    res = {}
+    g = torch.Generator().manual_seed(41)
+    for name, n, reps in (("one_step_1080p_latent", 48 * 8 * 68 * 120, 200), ("one_step_2e28", 1 << 28, 20)):
+        z = torch.randn(n, generator=g).to(torch.bfloat16).to(dev)
+        v = torch.randn(n, generator=g).to(torch.bfloat16).to(dev)
+        out = torch.empty(n, dtype=torch.float32, device=dev)
+        ms = _time_ms(torch, cur, lambda: fastvr.one_step_update(z, v, 0.8, out=out), reps)
+        gbs = n * 8 / (ms * 1e-3) / 1e9
+        res[name] = {"elements": n, "ms": round(ms, 5), "GB/s": round(gbs, 1),
+                     "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+        del z, v, out
+    return res
+
+
 def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     """ms/call and effective TFLOP/s of the other synthetic workloads: the
     480p-shaped and the wide sliding-window parallel calls, and the paper's
@@ -156,6 +178,7 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
                                  "note": "chunk 3 vs chunks 2-3, append of chunk 3 fused into the launch"}
     del ring_k, ring_v, qn, kn, vn, o, lse
     res["bwd_1080p"] = backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, 5)
+    res.update(one_step_update_timing(torch, fastvr, dev, cur))
     return res
 
 

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 3
+#define FASTVR_ABI_VERSION 4
 
 typedef enum {
   FASTVR_OK = 0,
@@ -183,6 +183,25 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
                                     const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
                                     int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
                                     int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream);
+
+/*
+ * One-step latent update (Sec. 3.2, Eq. 9, the update used at inference, Sec.
+ * 4.1): z_hat = z_lq - sigma * v, element by element over n elements.
+ *
+ *   z_lq    bf16 [n]   the LQ latent z_LQ (any layout; v and z_hat share it)
+ *   v       bf16 [n]   the velocity the DiT predicts at (z_LQ, tau)
+ *   z_hat   fp32 [n] (out_bf16 = 0) or bf16 [n] (out_bf16 = 1)   output
+ *   sigma   sigma_tau, the noise level of the starting timestep tau
+ * Each element is fma(-sigma, v, z_lq) in fp32 (the exact value rounded once);
+ * with out_bf16 = 1 that value is rounded to bf16 (nearest even).
+ *
+ * Preconditions (else FASTVR_ERR_INVALID_ARGUMENT): n >= 0; pointers non-NULL
+ * and 16-byte aligned; sigma finite; out_bf16 in {0, 1}; z_hat overlaps neither
+ * input, except that with out_bf16 = 1 it may be exactly z_lq or v (in place).
+ * n = 0: FASTVR_OK, nothing enqueued.
+ */
+fastvr_status fastvr_one_step_update(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma,
+                                     int32_t out_bf16, void* stream);
 
 /* Static string naming a status code ("FASTVR_OK", ...); never NULL. */
 const char* fastvr_status_string(fastvr_status s);

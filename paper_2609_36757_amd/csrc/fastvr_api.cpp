@@ -383,6 +383,35 @@ fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k
   return ok();
 }
 
+fastvr_status fastvr_one_step_update(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma,
+                                     int32_t out_bf16, void* stream) {
+  if (n < 0) return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size n = %lld", (long long)n);
+  if (!std::isfinite(sigma)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "sigma is not finite");
+  if (out_bf16 != 0 && out_bf16 != 1)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "out_bf16 must be 0 or 1 (got %d)", (int)out_bf16);
+  if (n == 0) return ok();
+  const void* ptrs[3] = {z_lq, v, z_hat};
+  const char* names[3] = {"z_lq", "v", "z_hat"};
+  for (int i = 0; i < 3; ++i) {
+    if (ptrs[i] == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is NULL", names[i]);
+    if (!aligned(ptrs[i], 16)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", names[i]);
+  }
+  int64_t in_bytes, out_bytes;
+  if (!mul_ok(n, 2, &in_bytes) || !mul_ok(n, out_bf16 ? 2 : 4, &out_bytes))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  // in place is allowed when the output has the input's element size and
+  // starts exactly at z_lq or v (each element is read before it is written)
+  for (int i = 0; i < 2; ++i) {
+    if (out_bf16 && z_hat == ptrs[i]) continue;
+    if (overlap(z_hat, out_bytes, ptrs[i], in_bytes))
+      return fail(FASTVR_ERR_INVALID_ARGUMENT, "z_hat overlaps %s", names[i]);
+  }
+  const hipError_t e = fastvr::launch_one_step(z_lq, v, z_hat, n, sigma, out_bf16 != 0,
+                                               static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "one_step launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 const char* fastvr_status_string(fastvr_status s) {
   switch (s) {
     case FASTVR_OK: return "FASTVR_OK";

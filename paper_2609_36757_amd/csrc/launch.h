@@ -82,6 +82,9 @@ constexpr int kBwdKeysPerItem = 128;
 BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len);
 hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream);
 
+hipError_t launch_one_step(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma, bool out_bf16,
+                           hipStream_t stream);
+
 hipError_t launch_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
                             int64_t B, int64_t H, int64_t d, int64_t capacity, int64_t cache_len,
                             int64_t n_new, hipStream_t stream);

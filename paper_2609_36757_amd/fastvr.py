@@ -19,7 +19,8 @@ ERR_CAPACITY = 3
 ERR_HIP = 4
 
 EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
-            "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
+            "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_one_step_update",
+            "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
 
 _i64 = ctypes.c_int64
 _vp = ctypes.c_void_p
@@ -55,6 +56,8 @@ def load() -> ctypes.CDLL:
     lib.fastvr_chunk_attn_bwd.restype = ctypes.c_int
     lib.fastvr_chunk_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64,
                                           _i64, _i64, _i64, _i64, ctypes.c_float, _vp]
+    lib.fastvr_one_step_update.restype = ctypes.c_int
+    lib.fastvr_one_step_update.argtypes = [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_int32, _vp]
     lib.fastvr_status_string.restype = ctypes.c_char_p
     lib.fastvr_status_string.argtypes = [ctypes.c_int]
     lib.fastvr_last_error.restype = ctypes.c_char_p
@@ -109,6 +112,10 @@ def bwd_raw(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chun
             window_chunks, scale, stream=0) -> int:
     return load().fastvr_chunk_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chunk_len,
                                         q_chunk_offset, window_chunks, scale, stream)
+
+
+def one_step_raw(z_lq, v, z_hat, n, sigma, out_bf16, stream=0) -> int:
+    return load().fastvr_one_step_update(z_lq, v, z_hat, n, sigma, out_bf16, stream)
 
 
 # ---------------------------------------------------------------------------
@@ -258,3 +265,28 @@ def chunk_attn_bwd(q, k, v, o, lse, dout, *, chunk_len: int, q_chunk_offset: int
                    dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), row_stats.data_ptr(), B, H, Nq, Nkv, d, chunk_len,
                    q_chunk_offset, window_chunks, scale, _stream_handle(stream)))
     return dq, dk, dv
+
+
+def one_step_update(z_lq, v, sigma: float, *, out=None, out_dtype=None, stream=None):
+    """One-step latent update z_hat = z_lq - sigma * v (FastVR Eq. 9).
+
+    z_lq, v: contiguous bf16 GPU tensors of one shape.  The result is float32
+    (default) or bfloat16 (``out_dtype=torch.bfloat16``; ``out`` may then be
+    z_lq or v itself, for an update in place)."""
+    import torch
+    for name, t in (("z_lq", z_lq), ("v", v)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor")
+    if v.shape != z_lq.shape:
+        raise ValueError(f"shape mismatch: z_lq {tuple(z_lq.shape)} v {tuple(v.shape)}")
+    if out_dtype is None:
+        out_dtype = out.dtype if out is not None else torch.float32
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be float32 or bfloat16")
+    if out is None:
+        out = torch.empty(z_lq.shape, dtype=out_dtype, device=z_lq.device)
+    if out.dtype != out_dtype or out.shape != z_lq.shape or not out.is_contiguous():
+        raise ValueError("out must be a contiguous tensor of z_lq's shape and dtype out_dtype")
+    _check(one_step_raw(z_lq.data_ptr(), v.data_ptr(), out.data_ptr(), z_lq.numel(), sigma,
+                        1 if out_dtype == torch.bfloat16 else 0, _stream_handle(stream)))
+    return out

@@ -14,7 +14,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 # Distinct fake addresses, 1 TiB apart, for calls that must fail validation:
 # every case below is rejected on the host before the HIP runtime is touched.
-Q, K, V, O, LSE, RK, RV, DO, DQ, DK, DV, RS = ((i + 1) << 40 for i in range(12))
+Q, K, V, O, LSE, RK, RV, DO, DQ, DK, DV, RS, Z, VEL, ZH = ((i + 1) << 40 for i in range(15))
 BIG = 1 << 62
 
 
@@ -40,7 +40,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 3
+    assert lib.fastvr_abi_version() == 4
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -241,6 +241,39 @@ def test_bwd_rejects(lib, kw, status, needle):
 @pytest.mark.parametrize("kw", [dict(B=0), dict(H=0), dict(Nq=0, Nkv=0)])
 def test_bwd_empty_is_ok(lib, kw):
     assert _bwd(**kw) == fastvr.OK
+
+
+OS_GOOD = dict(z=Z, v=VEL, out=ZH, n=1000, sigma=0.5, out_bf16=0)
+
+
+def _os(**kw):
+    a = dict(OS_GOOD)
+    a.update(kw)
+    return fastvr.one_step_raw(a["z"], a["v"], a["out"], a["n"], a["sigma"], a["out_bf16"], None)
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(z=None), "z_lq is NULL"),
+    (dict(v=None), "v is NULL"),
+    (dict(out=None), "z_hat is NULL"),
+    (dict(z=Z + 8), "aligned"),
+    (dict(out=ZH + 4), "aligned"),
+    (dict(n=-1), "negative size"),
+    (dict(sigma=float("nan")), "sigma"),
+    (dict(sigma=float("-inf")), "sigma"),
+    (dict(out_bf16=2), "out_bf16"),
+    (dict(out=Z), "z_hat overlaps z_lq"),               # fp32 output onto the bf16 input
+    (dict(out=Z + 1024, out_bf16=1), "z_hat overlaps z_lq"),
+    (dict(out=VEL + 16, out_bf16=1), "z_hat overlaps v"),
+])
+def test_one_step_rejects(lib, kw, needle):
+    assert _os(**kw) == fastvr.ERR_INVALID_ARGUMENT
+    assert needle in fastvr.last_error()
+
+
+def test_one_step_empty_is_ok(lib):
+    assert _os(n=0) == fastvr.OK
+    assert _os(n=0, z=None, v=None, out=None) == fastvr.OK
 
 
 def test_error_is_thread_local(lib):
