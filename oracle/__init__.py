@@ -19,3 +19,4 @@ from .chunk_attention import (  # noqa: F401
     visibility_mask,
 )
 from .one_step import one_step_update, target_velocity  # noqa: F401
+from .tiles import axis_weights, tile_axis, tile_blend, tile_gather  # noqa: F401

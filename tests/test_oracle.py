@@ -676,3 +676,78 @@ def test_one_step_pin_catches_a_sign_error(monkeypatch):
     u = oracle.target_velocity(z_lq, z_hq, 0.5)
     bad = os_mod._f64(z_lq) + 0.5 * u
     assert np.abs(bad - z_hq).max() > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# spatial tiles (Sec. 4.1, Inference): placement, gather, blend
+# ---------------------------------------------------------------------------
+
+def test_tile_blend_hand_example():
+    """tests/golden/tile_blend_example.csv: two overlapping tiles along x."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "tile_blend_example.csv")
+    rows = [[int(v) for v in line.split(",")] for line in open(path)
+            if line.strip() and not line.startswith("#") and not line.startswith("x,")]
+    assert oracle.tile_axis(6, 4, 2) == ([0, 2], 4)
+    tiles = np.zeros((1, 2, 1, 1, 4, 1))
+    tiles[0, 0, 0, 0, :, 0] = [1, 2, 3, 4]
+    tiles[0, 1, 0, 0, :, 0] = [10, 20, 30, 40]
+    out = oracle.tile_blend(tiles, 1, 6, 4, 2)
+    for x, num, den in rows:
+        assert abs(out[0, 0, 0, x, 0] - num / den) < 1e-14
+
+
+@pytest.mark.parametrize("size,tile,overlap", [(68, 64, 16), (120, 64, 16), (200, 64, 16), (30, 64, 16),
+                                               (65, 64, 8), (128, 64, 0), (1000, 64, 32), (7, 4, 3)])
+def test_tile_axis_properties(size, tile, overlap):
+    """Origins start at 0, end flush with the grid, are non-decreasing, cover every
+    position, neighbours overlap by at least `overlap`, and no smaller number of
+    tiles could satisfy that (a tile count one lower would force a smaller overlap)."""
+    origins, L = oracle.tile_axis(size, tile, overlap)
+    n = len(origins)
+    assert L == min(tile, size) and origins[0] == 0 and origins[-1] == size - L
+    covered = np.zeros(size, dtype=bool)
+    for a in origins:
+        covered[a:a + L] = True
+    assert covered.all()
+    for a, b in zip(origins, origins[1:]):
+        assert 0 < b - a and a + L - b >= overlap
+    if n > 2:
+        assert (size - L) / (n - 2) > L - overlap
+
+
+def test_tile_gather_then_blend_is_identity():
+    """Blending the tiles of a field returns the field (the weights are positive
+    and normalised), for several geometries."""
+    rng = np.random.default_rng(210)
+    for (Hg, Wg, tile, ov) in [(68, 120, 64, 16), (30, 52, 64, 16), (40, 33, 16, 5), (9, 9, 4, 3)]:
+        x = rng.standard_normal((2, 3, Hg, Wg, 4))
+        t = oracle.tile_gather(x, tile, ov)
+        np.testing.assert_allclose(oracle.tile_blend(t, Hg, Wg, tile, ov), x, rtol=0, atol=1e-12)
+
+
+def test_tile_closed_forms():
+    # constant tiles blend to the constant; disjoint tiles (overlap 0) reassemble exactly
+    t = np.full((1, 6, 2, 64, 64, 3), 2.5)
+    np.testing.assert_array_equal(oracle.tile_blend(t, 68, 120, 64, 16), np.full((1, 2, 68, 120, 3), 2.5))
+    rng = np.random.default_rng(211)
+    x = rng.standard_normal((1, 2, 8, 12, 2))
+    t = oracle.tile_gather(x, 4, 0)
+    assert t.shape == (1, 6, 2, 4, 4, 2)
+    np.testing.assert_array_equal(t[0, 4], x[0, :, 4:8, 4:8])   # tile (1, 1)
+    np.testing.assert_array_equal(oracle.tile_blend(t, 8, 12, 4, 0), x)
+    np.testing.assert_array_equal(oracle.axis_weights(6, 2), [1, 2, 2, 2, 2, 1])
+
+
+def test_tile_pins_catch_a_missing_normalisation(monkeypatch):
+    """A blend without the division by the weight sum fails the identity pin."""
+    import oracle.tiles as ot
+    rng = np.random.default_rng(212)
+    x = rng.standard_normal((1, 1, 20, 20, 1))
+    t = oracle.tile_gather(x, 8, 4)
+    oy, L = ot.tile_axis(20, 8, 4)
+    w = ot.axis_weights(L, 4)
+    acc = np.zeros((20, 20))
+    for ty, ay in enumerate(oy):
+        for tx, ax in enumerate(oy):
+            acc[ay:ay + L, ax:ax + L] += np.outer(w, w) * t[0, ty * len(oy) + tx, 0, :, :, 0]
+    assert np.abs(acc - x[0, 0, :, :, 0]).max() > 1e-3
