@@ -11,8 +11,9 @@ value = effective (unmasked) TFLOP/s of the whole step: 4 * d * visible pairs
 
 After the timed steps (and outside them) it reports ms/call and TFLOP/s of
 the 480p-shaped and wide sliding-window calls, of the W = 1 ring-cache
-streaming step, of the backward of the 1080p call and of the one-step latent
-update (``other_workloads``), then the fp64 oracle baseline.
+streaming step, of the backward of the 1080p call, of the one-step latent
+update and of tiled inference with overlapping 64 x 64 latent tiles
+(``other_workloads``), then the fp64 oracle baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
 """
@@ -140,6 +141,48 @@ def one_step_update_timing(torch, fastvr, dev, cur):
     return res
 
 
+def tiled_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w):
+    """Tiled inference on the 1080p sequence with the paper's overlapping 64 x 64
+    latent tiles (overlap 16): gather of the q, k, v tokens (8 latent frames x 68
+    x 120 positions, H * d = 1536 channels) into 2 x 3 tiles, one chunk-causal
+    attention call over the tile batch (6 x 32768 tokens, chunks of 2 frames =
+    8192 tokens), the blend of the per-tile outputs back onto the grid, and the
+    blend of 48-channel velocity tiles fused with the one-step update of Eq. 9."""
+    T, Hg, Wg, C = 8, 68, 120, w.H * w.d
+    tile, ov = 64, 16
+    grid = lambda t: t.view(w.B, T, Hg, Wg, C)
+    qg, kg, vg = grid(qd), grid(kd), grid(vd)
+    tiles = [fastvr.tile_gather(t, tile=tile, overlap=ov) for t in (qg, kg, vg)]
+    Bt, nt, _, Ly, Lx, _ = tiles[0].shape
+    ms_g = _time_ms(torch, cur, lambda: [fastvr.tile_gather(t, tile=tile, overlap=ov, out=o)
+                                         for t, o in zip((qg, kg, vg), tiles)], 10)
+    N, L = T * Ly * Lx, 2 * Ly * Lx
+    tok = lambda t: t.view(Bt * nt, N, w.H, w.d)
+    o = torch.empty((Bt * nt, N, w.H, w.d), dtype=torch.float32, device=dev)
+    lse = torch.empty((Bt * nt, w.H, N), dtype=torch.float32, device=dev)
+    ms_a = _time_ms(torch, cur, lambda: fastvr.chunk_attn(tok(tiles[0]), tok(tiles[1]), tok(tiles[2]), chunk_len=L,
+                                                          window_chunks=w.window_chunks, scale=w.scale, out=o,
+                                                          lse=lse), 5)
+    f_a = metrics.effective_flops(Bt * nt, w.H, w.d, N, N, L, 0, w.window_chunks)
+    out = torch.empty((w.B, T, Hg, Wg, C), dtype=torch.float32, device=dev)
+    o6 = o.view(Bt, nt, T, Ly, Lx, C)
+    ms_b = _time_ms(torch, cur, lambda: fastvr.tile_blend(o6, Hg, Wg, tile=tile, overlap=ov, out=out), 10)
+    g = torch.Generator().manual_seed(43)
+    vt = torch.randn((w.B, nt, T, Ly, Lx, 48), generator=g).to(dev)
+    z = torch.randn((w.B, T, Hg, Wg, 48), generator=g).to(torch.bfloat16).to(dev)
+    zh = torch.empty((w.B, T, Hg, Wg, 48), dtype=torch.float32, device=dev)
+    ms_u = _time_ms(torch, cur, lambda: fastvr.tile_blend(vt, Hg, Wg, tile=tile, overlap=ov, z_lq=z, sigma=0.8,
+                                                          out=zh), 50)
+    gb = lambda nbytes, ms: round(nbytes / (ms * 1e-3) / 1e9, 1)
+    tile_bytes = tiles[0].numel() * 2
+    return {"tiles": f"{nt} ({Ly} x {Lx}) per frame, {N} tokens per tile",
+            "gather_qkv_ms": round(ms_g, 4), "gather_GB/s": gb(3 * 2 * tile_bytes, ms_g),
+            "attention_ms": round(ms_a, 4), "attention_tflops": round(f_a / (ms_a * 1e-3) / 1e12, 2),
+            "blend_o_ms": round(ms_b, 4), "blend_GB/s": gb(o.numel() * 4 + out.numel() * 4, ms_b),
+            "blend_update_latent_ms": round(ms_u, 5),
+            "blend_update_GB/s": gb(vt.numel() * 4 + z.numel() * 2 + zh.numel() * 4, ms_u)}
+
+
 def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     """ms/call and effective TFLOP/s of the other synthetic workloads: the
     480p-shaped and the wide sliding-window parallel calls, and the paper's
@@ -179,6 +222,7 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     del ring_k, ring_v, qn, kn, vn, o, lse
     res["bwd_1080p"] = backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, 5)
     res.update(one_step_update_timing(torch, fastvr, dev, cur))
+    res["tiled_1080p"] = tiled_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w)
     return res
 
 

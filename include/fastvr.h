@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 4
+#define FASTVR_ABI_VERSION 5
 
 typedef enum {
   FASTVR_OK = 0,
@@ -202,6 +202,51 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
  */
 fastvr_status fastvr_one_step_update(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma,
                                      int32_t out_bf16, void* stream);
+
+/*
+ * Spatial tiles for tiled inference (Sec. 3 overview: one DiT pass per temporal
+ * chunk and spatial tile; Sec. 4.1, Inference: overlapping 64 x 64 latent tiles).
+ * The paper does not state the overlap, the placement or the blend; this library
+ * takes the following, for fields laid out channels-last x[b, t, y, x, c] over a
+ * grid of Hg x Wg positions and T frames (tiles span every frame and cut both
+ * spatial axes the same way):
+ *  - along an axis of `size` positions: tile length L = min(tile, size);
+ *    n = 1 if size <= tile, else ceil((size - overlap) / (tile - overlap)) tiles
+ *    at origins a_k = (k (size - L) + (n - 1) / 2) / (n - 1) (integer division):
+ *    evenly spaced, a_0 = 0, a_{n-1} = size - L, neighbours overlapping by at
+ *    least `overlap`;
+ *  - tile (ty, tx) has index ty * nx + tx; a tile tensor is
+ *    [B, ny * nx, T, Ly, Lx, C], so a tile batch feeds fastvr_chunk_attn_fwd
+ *    directly (batch B * ny * nx, Nq = T * Ly * Lx tokens, chunk_len =
+ *    frames per chunk * Ly * Lx);
+ *  - blend: position i of a tile has the axis weight min(i + 1, L - i, R),
+ *    R = max(overlap, 1); a tile's weight is the product of its two axis
+ *    weights, and the blended value is the weight-normalised sum over the tiles
+ *    that cover the position (fp32, tiles in index order).
+ * Common preconditions (else FASTVR_ERR_INVALID_ARGUMENT unless noted): sizes
+ * >= 0; tile >= 1 and 0 <= overlap < tile; tile <= 4096 (else
+ * FASTVR_ERR_UNSUPPORTED); Wg * C < 2^31 (else FASTVR_ERR_UNSUPPORTED); tensors
+ * contiguous, pointers 16-byte aligned (z_lq: 8-byte); outputs overlap no
+ * input.  An empty field (any size 0): FASTVR_OK, nothing enqueued.
+ */
+
+/* Host only: number of tiles and tile length along one axis of `size` >= 1. */
+fastvr_status fastvr_tile_axis(int64_t size, int64_t tile, int64_t overlap, int64_t* n_tiles, int64_t* tile_len);
+
+/* tiles bf16 [B, ny*nx, T, Ly, Lx, C] <- x bf16 [B, T, Hg, Wg, C]; C a multiple of 8. */
+fastvr_status fastvr_tile_gather(const void* x, void* tiles, int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C,
+                                 int64_t tile, int64_t overlap, void* stream);
+
+/* out fp32 [B, T, Hg, Wg, C] <- blend of tiles fp32 [B, ny*nx, T, Ly, Lx, C]; C a multiple of 4. */
+fastvr_status fastvr_tile_blend(const float* tiles, float* out, int64_t B, int64_t T, int64_t Hg, int64_t Wg,
+                                int64_t C, int64_t tile, int64_t overlap, void* stream);
+
+/* The blend fused with the one-step update of Eq. 9 (Sec. 3.2):
+ * z_hat fp32 [B, T, Hg, Wg, C] = z_lq - sigma * blend(v_tiles), z_lq bf16 of the
+ * same shape (each element fma(-sigma, blend, z) in fp32); sigma finite. */
+fastvr_status fastvr_tile_blend_update(const float* v_tiles, const void* z_lq, float* z_hat, float sigma, int64_t B,
+                                       int64_t T, int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t overlap,
+                                       void* stream);
 
 /* Static string naming a status code ("FASTVR_OK", ...); never NULL. */
 const char* fastvr_status_string(fastvr_status s);

@@ -412,6 +412,109 @@ fastvr_status fastvr_one_step_update(const void* z_lq, const void* v, void* z_ha
   return ok();
 }
 
+}  // extern "C"
+
+namespace {
+
+// Shared checks of the tile entry points; fills the two axes and the element
+// counts of the field and of the tile tensor.
+fastvr_status tile_check(int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t tile_overlap,
+                         int64_t c_multiple, fastvr::TileAxis* ay, fastvr::TileAxis* ax, int64_t* field_elems,
+                         int64_t* tile_elems) {
+  if (B < 0 || T < 0 || Hg < 0 || Wg < 0 || C < 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld T=%lld Hg=%lld Wg=%lld C=%lld)", (long long)B,
+                (long long)T, (long long)Hg, (long long)Wg, (long long)C);
+  if (tile < 1 || tile_overlap < 0 || tile_overlap >= tile)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "need tile >= 1 and 0 <= overlap < tile (tile=%lld overlap=%lld)",
+                (long long)tile, (long long)tile_overlap);
+  if (tile > fastvr::kMaxTile)
+    return fail(FASTVR_ERR_UNSUPPORTED, "tile %lld > %lld", (long long)tile, (long long)fastvr::kMaxTile);
+  if (C % c_multiple != 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "C = %lld is not a multiple of %lld", (long long)C, (long long)c_multiple);
+  *field_elems = 0;
+  *tile_elems = 0;
+  if (B == 0 || T == 0 || Hg == 0 || Wg == 0 || C == 0) return FASTVR_OK;
+  *ay = fastvr::tile_axis(Hg, tile, tile_overlap);
+  *ax = fastvr::tile_axis(Wg, tile, tile_overlap);
+  int64_t f, t;
+  if (!mul_ok(B, T, &f) || !mul_ok(f, Hg, &f) || !mul_ok(f, Wg, &f) || !mul_ok(f, C, &f) ||
+      !mul_ok(B, ay->n * ax->n, &t) || !mul_ok(t, T, &t) || !mul_ok(t, ay->len * ax->len, &t) || !mul_ok(t, C, &t) ||
+      !mul_ok(t, 4, &t) || !mul_ok(f, 4, &f))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+  if (Hg > INT32_MAX || Wg > INT32_MAX || T > INT32_MAX || Wg * C > INT32_MAX)
+    return fail(FASTVR_ERR_UNSUPPORTED, "a grid row must hold fewer than 2^31 elements");
+  *field_elems = f / 4;
+  *tile_elems = t / 4;
+  return FASTVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fastvr_status fastvr_tile_axis(int64_t size, int64_t tile, int64_t tile_overlap, int64_t* n_tiles, int64_t* tile_len) {
+  if (n_tiles == nullptr || tile_len == nullptr)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "n_tiles or tile_len is NULL");
+  if (size < 1 || tile < 1 || tile_overlap < 0 || tile_overlap >= tile)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "need size >= 1, tile >= 1 and 0 <= overlap < tile");
+  const fastvr::TileAxis a = fastvr::tile_axis(size, tile, tile_overlap);
+  *n_tiles = a.n;
+  *tile_len = a.len;
+  return ok();
+}
+
+fastvr_status fastvr_tile_gather(const void* x, void* tiles, int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C,
+                                 int64_t tile, int64_t tile_overlap, void* stream) {
+  fastvr::TileAxis ay{}, ax{};
+  int64_t fe, te;
+  fastvr_status s = tile_check(B, T, Hg, Wg, C, tile, tile_overlap, 8, &ay, &ax, &fe, &te);
+  if (s != FASTVR_OK) return s;
+  if (fe == 0) return ok();
+  if (x == nullptr || tiles == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "x or tiles is NULL");
+  if (!aligned(x, 16) || !aligned(tiles, 16))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "x or tiles is not 16-byte aligned");
+  if (overlap(x, fe * 2, tiles, te * 2)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "tiles overlaps x");
+  const hipError_t e =
+      fastvr::launch_tile_gather(x, tiles, B, T, Hg, Wg, C, tile, tile_overlap, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "tile_gather launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+static fastvr_status blend_impl(const float* tiles, const void* z_lq, float* out, float sigma, int64_t B, int64_t T,
+                                int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t tile_overlap, void* stream) {
+  fastvr::TileAxis ay{}, ax{};
+  int64_t fe, te;
+  fastvr_status s = tile_check(B, T, Hg, Wg, C, tile, tile_overlap, 4, &ay, &ax, &fe, &te);
+  if (s != FASTVR_OK) return s;
+  if (!std::isfinite(sigma)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "sigma is not finite");
+  if (fe == 0) return ok();
+  if (tiles == nullptr || out == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "tiles or out is NULL");
+  if (!aligned(tiles, 16) || !aligned(out, 16))
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "tiles or out is not 16-byte aligned");
+  if (overlap(out, fe * 4, tiles, te * 4)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "out overlaps tiles");
+  if (z_lq != nullptr) {
+    if (!aligned(z_lq, 8)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "z_lq is not 8-byte aligned");
+    if (overlap(out, fe * 4, z_lq, fe * 2)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "out overlaps z_lq");
+  }
+  const hipError_t e = fastvr::launch_tile_blend(tiles, z_lq, out, sigma, B, T, Hg, Wg, C, tile, tile_overlap,
+                                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "tile_blend launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+fastvr_status fastvr_tile_blend(const float* tiles, float* out, int64_t B, int64_t T, int64_t Hg, int64_t Wg,
+                                int64_t C, int64_t tile, int64_t tile_overlap, void* stream) {
+  return blend_impl(tiles, nullptr, out, 0.f, B, T, Hg, Wg, C, tile, tile_overlap, stream);
+}
+
+fastvr_status fastvr_tile_blend_update(const float* v_tiles, const void* z_lq, float* z_hat, float sigma, int64_t B,
+                                       int64_t T, int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t tile_overlap,
+                                       void* stream) {
+  if (z_lq == nullptr && B > 0 && T > 0 && Hg > 0 && Wg > 0 && C > 0)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "z_lq is NULL");
+  return blend_impl(v_tiles, z_lq, z_hat, sigma, B, T, Hg, Wg, C, tile, tile_overlap, stream);
+}
+
 const char* fastvr_status_string(fastvr_status s) {
   switch (s) {
     case FASTVR_OK: return "FASTVR_OK";

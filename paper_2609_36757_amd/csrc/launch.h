@@ -85,6 +85,18 @@ hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream);
 hipError_t launch_one_step(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma, bool out_bf16,
                            hipStream_t stream);
 
+// Spatial tiles: tiles and tile length along one axis (host side, shared by the
+// C ABI's checks and the launchers); n = 0 for an invalid geometry.
+struct TileAxis {
+  int64_t n, len;
+};
+constexpr int64_t kMaxTile = 4096;  // integer blend weights up to kMaxTile^2 stay exact in fp32
+TileAxis tile_axis(int64_t size, int64_t tile, int64_t overlap);
+hipError_t launch_tile_gather(const void* x, void* tiles, int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C,
+                              int64_t tile, int64_t overlap, hipStream_t stream);
+hipError_t launch_tile_blend(const float* tiles, const void* z_lq, float* out, float sigma, int64_t B, int64_t T,
+                             int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t overlap, hipStream_t stream);
+
 hipError_t launch_kv_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new,
                             int64_t B, int64_t H, int64_t d, int64_t capacity, int64_t cache_len,
                             int64_t n_new, hipStream_t stream);

@@ -1,0 +1,163 @@
+// Spatial tiling of the latent for tiled inference (FastVR, Sec. 3 overview and
+// Sec. 4.1: the DiT runs once per temporal chunk and overlapping 64 x 64 latent
+// tile).  Fields are channels-last, x[b, t, y, x, c]; tiles span every frame and
+// cut the two spatial axes identically:
+//  * placement along an axis of `size`: tile length L = min(tile, size),
+//    n = 1 if size <= tile else ceil((size - overlap) / (tile - overlap)) tiles
+//    at evenly spaced origins a_k = (k (size - L) + (n - 1) / 2) / (n - 1)
+//    (integer division), so a_0 = 0, a_{n-1} = size - L and neighbours overlap
+//    by at least `overlap`;
+//  * gather: tiles[b, ty * nx + tx, t, iy, ix, c] = x[b, t, a_ty + iy, a_tx + ix, c];
+//  * blend: axis weight of tile position i is min(i + 1, L - i, R), R =
+//    max(overlap, 1); a tile's weight at a position is the product of its two
+//    axis weights, and the field is the weight-normalised sum over the tiles
+//    covering the position.  Optionally fused with the one-step update of
+//    Eq. 9: z_hat = z_LQ - sigma * blend(v tiles).
+// Both kernels are bound by HBM bandwidth.  The gather copies each tile row (a
+// contiguous run in source and destination) with 16-byte vectors; the blend
+// gathers, for each output element, the few tiles covering it (no atomics).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gfx950_ops.h"
+#include "launch.h"
+
+namespace fastvr {
+namespace {
+
+using namespace dev;
+
+constexpr int kThreads = 256;
+
+struct Axis {
+  int n, L, span;  // tiles, tile length, size - L
+};
+
+__device__ __forceinline__ int origin(const Axis& a, int k) {
+  return a.n == 1 ? 0 : (int)(((int64_t)k * a.span + (a.n - 1) / 2) / (a.n - 1));
+}
+
+__device__ __forceinline__ int axis_weight(int i, int L, int R) {
+  const int m = (i + 1 < L - i) ? i + 1 : L - i;
+  return m < R ? m : R;
+}
+
+// One tile row (b, tile, t, iy) per loop step of a workgroup; 16-byte units.
+__global__ __launch_bounds__(kThreads) void tile_gather_kernel(const u32x4* __restrict__ x, u32x4* __restrict__ tiles,
+                                                               int T, int Hg, int Wg, int C16, Axis ay, Axis ax,
+                                                               int64_t n_rows) {
+  const int64_t row_units = (int64_t)ax.L * C16;
+  for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
+    // r = ((b * nt + tile) * T + t) * Ly + iy  (wave-uniform)
+    int64_t q = r;
+    const int iy = (int)(q % ay.L);
+    q /= ay.L;
+    const int t = (int)(q % T);
+    q /= T;
+    const int nt = ay.n * ax.n;
+    const int tile = (int)(q % nt);
+    const int64_t b = q / nt;
+    const int ty = tile / ax.n, tx = tile - ty * ax.n;
+    const int y = origin(ay, ty) + iy, x0 = origin(ax, tx);
+    const u32x4* src = x + (((b * T + t) * Hg + y) * (int64_t)Wg + x0) * C16;
+    u32x4* dst = tiles + r * row_units;
+    for (int64_t u = threadIdx.x; u < row_units; u += kThreads) __builtin_nontemporal_store(src[u], dst + u);
+  }
+}
+
+// One output row (b, t, y) per loop step of a workgroup; 4 channels (16 bytes of
+// fp32) per thread and step.  With Z (fused Eq. 9) the output is
+// z - sigma * blend, z bf16.
+template <bool Z>
+__global__ __launch_bounds__(kThreads) void tile_blend_kernel(const float* __restrict__ tiles,
+                                                              const uint16_t* __restrict__ z, float* __restrict__ out,
+                                                              float neg_sigma, int T, int Hg, int Wg, int C, Axis ay,
+                                                              Axis ax, int R, int64_t n_rows) {
+  const int C4 = C / 4;
+  const int row_units = Wg * C4;
+  const int nt = ay.n * ax.n;
+  for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
+    // r = (b * T + t) * Hg + y  (wave-uniform)
+    const int y = (int)(r % Hg);
+    const int64_t bt = r / Hg;
+    const int t = (int)(bt % T);
+    const int64_t b = bt / T;
+    for (int u = threadIdx.x; u < row_units; u += kThreads) {
+      const int xg = u / C4, c4 = u - (u / C4) * C4;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      float wsum = 0.f;
+      for (int ty = 0; ty < ay.n; ++ty) {
+        const int iy = y - origin(ay, ty);
+        if (iy < 0 || iy >= ay.L) continue;
+        const int wy = axis_weight(iy, ay.L, R);
+        for (int tx = 0; tx < ax.n; ++tx) {
+          const int ix = xg - origin(ax, tx);
+          if (ix < 0 || ix >= ax.L) continue;
+          const float w = (float)(wy * axis_weight(ix, ax.L, R));
+          const int64_t tr = ((b * nt + ty * ax.n + tx) * T + t) * ay.L + iy;  // tile row
+          const f32x4 v = *reinterpret_cast<const f32x4*>(tiles + (tr * ax.L + ix) * C + 4 * c4);
+          acc.x = __builtin_fmaf(w, v.x, acc.x);
+          acc.y = __builtin_fmaf(w, v.y, acc.y);
+          acc.z = __builtin_fmaf(w, v.z, acc.z);
+          acc.w = __builtin_fmaf(w, v.w, acc.w);
+          wsum += w;
+        }
+      }
+      f32x4 res = {acc.x / wsum, acc.y / wsum, acc.z / wsum, acc.w / wsum};
+      const int64_t o = (r * Wg + xg) * C + 4 * c4;
+      if (Z) {
+        const uint64_t zz = *reinterpret_cast<const uint64_t*>(z + o);
+        const __bf16* zb = reinterpret_cast<const __bf16*>(&zz);
+        res.x = __builtin_fmaf(neg_sigma, res.x, (float)zb[0]);
+        res.y = __builtin_fmaf(neg_sigma, res.y, (float)zb[1]);
+        res.z = __builtin_fmaf(neg_sigma, res.z, (float)zb[2]);
+        res.w = __builtin_fmaf(neg_sigma, res.w, (float)zb[3]);
+      }
+      __builtin_nontemporal_store(res, reinterpret_cast<f32x4*>(out + o));
+    }
+  }
+}
+
+Axis make_axis(int64_t size, int64_t tile, int64_t overlap) {
+  const TileAxis t = tile_axis(size, tile, overlap);
+  return Axis{(int)t.n, (int)t.len, (int)(size - t.len)};
+}
+
+unsigned grid_for(int64_t rows) { return (unsigned)(rows < 8192 ? (rows < 1 ? 1 : rows) : 8192); }
+
+}  // namespace
+
+TileAxis tile_axis(int64_t size, int64_t tile, int64_t overlap) {
+  TileAxis a{};
+  if (size < 1 || tile < 1 || overlap < 0 || overlap >= tile) return a;
+  a.len = size < tile ? size : tile;
+  a.n = size <= tile ? 1 : (size - overlap + (tile - overlap) - 1) / (tile - overlap);
+  return a;
+}
+
+hipError_t launch_tile_gather(const void* x, void* tiles, int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C,
+                              int64_t tile, int64_t overlap, hipStream_t stream) {
+  const Axis ay = make_axis(Hg, tile, overlap), ax = make_axis(Wg, tile, overlap);
+  const int64_t rows = B * ay.n * ax.n * T * ay.L;
+  hipLaunchKernelGGL(tile_gather_kernel, dim3(grid_for(rows)), dim3(kThreads), 0, stream,
+                     static_cast<const u32x4*>(x), static_cast<u32x4*>(tiles), (int)T, (int)Hg, (int)Wg, (int)(C / 8),
+                     ay, ax, rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_tile_blend(const float* tiles, const void* z_lq, float* out, float sigma, int64_t B, int64_t T,
+                             int64_t Hg, int64_t Wg, int64_t C, int64_t tile, int64_t overlap, hipStream_t stream) {
+  const Axis ay = make_axis(Hg, tile, overlap), ax = make_axis(Wg, tile, overlap);
+  const int64_t rows = B * T * Hg;
+  const int R = overlap > 1 ? (int)overlap : 1;
+  if (z_lq != nullptr)
+    hipLaunchKernelGGL(tile_blend_kernel<true>, dim3(grid_for(rows)), dim3(kThreads), 0, stream, tiles,
+                       static_cast<const uint16_t*>(z_lq), out, -sigma, (int)T, (int)Hg, (int)Wg, (int)C, ay, ax, R,
+                       rows);
+  else
+    hipLaunchKernelGGL(tile_blend_kernel<false>, dim3(grid_for(rows)), dim3(kThreads), 0, stream, tiles, nullptr,
+                       out, 0.f, (int)T, (int)Hg, (int)Wg, (int)C, ay, ax, R, rows);
+  return hipGetLastError();
+}
+
+}  // namespace fastvr

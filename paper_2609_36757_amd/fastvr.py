@@ -20,6 +20,7 @@ ERR_HIP = 4
 
 EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
             "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_one_step_update",
+            "fastvr_tile_axis", "fastvr_tile_gather", "fastvr_tile_blend", "fastvr_tile_blend_update",
             "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
 
 _i64 = ctypes.c_int64
@@ -58,6 +59,15 @@ def load() -> ctypes.CDLL:
                                           _i64, _i64, _i64, _i64, ctypes.c_float, _vp]
     lib.fastvr_one_step_update.restype = ctypes.c_int
     lib.fastvr_one_step_update.argtypes = [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_int32, _vp]
+    lib.fastvr_tile_axis.restype = ctypes.c_int
+    lib.fastvr_tile_axis.argtypes = [_i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
+    lib.fastvr_tile_gather.restype = ctypes.c_int
+    lib.fastvr_tile_gather.argtypes = [_vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _vp]
+    lib.fastvr_tile_blend.restype = ctypes.c_int
+    lib.fastvr_tile_blend.argtypes = [_vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _vp]
+    lib.fastvr_tile_blend_update.restype = ctypes.c_int
+    lib.fastvr_tile_blend_update.argtypes = [_vp, _vp, _vp, ctypes.c_float, _i64, _i64, _i64, _i64, _i64, _i64,
+                                             _i64, _vp]
     lib.fastvr_status_string.restype = ctypes.c_char_p
     lib.fastvr_status_string.argtypes = [ctypes.c_int]
     lib.fastvr_last_error.restype = ctypes.c_char_p
@@ -116,6 +126,25 @@ def bwd_raw(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chun
 
 def one_step_raw(z_lq, v, z_hat, n, sigma, out_bf16, stream=0) -> int:
     return load().fastvr_one_step_update(z_lq, v, z_hat, n, sigma, out_bf16, stream)
+
+
+def tile_axis(size: int, tile: int, overlap: int):
+    """(number of tiles, tile length) along one axis, as the library places them."""
+    n, L = _i64(0), _i64(0)
+    _check(load().fastvr_tile_axis(size, tile, overlap, ctypes.byref(n), ctypes.byref(L)))
+    return n.value, L.value
+
+
+def tile_gather_raw(x, tiles, B, T, Hg, Wg, C, tile, overlap, stream=0) -> int:
+    return load().fastvr_tile_gather(x, tiles, B, T, Hg, Wg, C, tile, overlap, stream)
+
+
+def tile_blend_raw(tiles, out, B, T, Hg, Wg, C, tile, overlap, stream=0) -> int:
+    return load().fastvr_tile_blend(tiles, out, B, T, Hg, Wg, C, tile, overlap, stream)
+
+
+def tile_blend_update_raw(v_tiles, z_lq, z_hat, sigma, B, T, Hg, Wg, C, tile, overlap, stream=0) -> int:
+    return load().fastvr_tile_blend_update(v_tiles, z_lq, z_hat, sigma, B, T, Hg, Wg, C, tile, overlap, stream)
 
 
 # ---------------------------------------------------------------------------
@@ -289,4 +318,53 @@ def one_step_update(z_lq, v, sigma: float, *, out=None, out_dtype=None, stream=N
         raise ValueError("out must be a contiguous tensor of z_lq's shape and dtype out_dtype")
     _check(one_step_raw(z_lq.data_ptr(), v.data_ptr(), out.data_ptr(), z_lq.numel(), sigma,
                         1 if out_dtype == torch.bfloat16 else 0, _stream_handle(stream)))
+    return out
+
+
+def _tile_shape(B, T, Hg, Wg, C, tile, overlap):
+    ny, Ly = tile_axis(Hg, tile, overlap)
+    nx, Lx = tile_axis(Wg, tile, overlap)
+    return (B, ny * nx, T, Ly, Lx, C)
+
+
+def tile_gather(x, *, tile: int = 64, overlap: int = 16, out=None, stream=None):
+    """Overlapping spatial tiles of a channels-last bf16 field x [B, T, Hg, Wg, C]
+    -> [B, ny * nx, T, Ly, Lx, C] (placement as in include/fastvr.h)."""
+    import torch
+    if x.dtype != torch.bfloat16 or not x.is_cuda or not x.is_contiguous() or x.dim() != 5:
+        raise ValueError("x must be a contiguous bfloat16 GPU tensor [B, T, Hg, Wg, C]")
+    B, T, Hg, Wg, C = x.shape
+    shape = _tile_shape(B, T, Hg, Wg, C, tile, overlap)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.bfloat16, device=x.device)
+    if out.dtype != torch.bfloat16 or tuple(out.shape) != shape or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous bfloat16 tensor of shape {shape}")
+    _check(tile_gather_raw(x.data_ptr(), out.data_ptr(), B, T, Hg, Wg, C, tile, overlap, _stream_handle(stream)))
+    return out
+
+
+def tile_blend(tiles, Hg: int, Wg: int, *, tile: int = 64, overlap: int = 16, z_lq=None, sigma: float = 0.0,
+               out=None, stream=None):
+    """Weight-normalised blend of fp32 tiles [B, ny * nx, T, Ly, Lx, C] into the
+    field [B, T, Hg, Wg, C] (fp32).  With z_lq (bf16 [B, T, Hg, Wg, C]) the result
+    is the one-step update z_lq - sigma * blend (Eq. 9), fused."""
+    import torch
+    if tiles.dtype != torch.float32 or not tiles.is_cuda or not tiles.is_contiguous() or tiles.dim() != 6:
+        raise ValueError("tiles must be a contiguous float32 GPU tensor [B, ny*nx, T, Ly, Lx, C]")
+    B, _, T, _, _, C = tiles.shape
+    if tuple(tiles.shape) != _tile_shape(B, T, Hg, Wg, C, tile, overlap):
+        raise ValueError("tiles do not match the grid, tile and overlap")
+    shape = (B, T, Hg, Wg, C)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=tiles.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != shape or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous float32 tensor of shape {shape}")
+    st = _stream_handle(stream)
+    if z_lq is None:
+        _check(tile_blend_raw(tiles.data_ptr(), out.data_ptr(), B, T, Hg, Wg, C, tile, overlap, st))
+    else:
+        if z_lq.dtype != torch.bfloat16 or tuple(z_lq.shape) != shape or not z_lq.is_contiguous():
+            raise ValueError(f"z_lq must be a contiguous bfloat16 tensor of shape {shape}")
+        _check(tile_blend_update_raw(tiles.data_ptr(), z_lq.data_ptr(), out.data_ptr(), sigma, B, T, Hg, Wg, C, tile,
+                                     overlap, st))
     return out

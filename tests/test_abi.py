@@ -14,7 +14,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 
 # Distinct fake addresses, 1 TiB apart, for calls that must fail validation:
 # every case below is rejected on the host before the HIP runtime is touched.
-Q, K, V, O, LSE, RK, RV, DO, DQ, DK, DV, RS, Z, VEL, ZH = ((i + 1) << 40 for i in range(15))
+Q, K, V, O, LSE, RK, RV, DO, DQ, DK, DV, RS, Z, VEL, ZH, X, TL, OUT = ((i + 1) << 40 for i in range(18))
 BIG = 1 << 62
 
 
@@ -40,7 +40,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 4
+    assert lib.fastvr_abi_version() == 5
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -274,6 +274,73 @@ def test_one_step_rejects(lib, kw, needle):
 def test_one_step_empty_is_ok(lib):
     assert _os(n=0) == fastvr.OK
     assert _os(n=0, z=None, v=None, out=None) == fastvr.OK
+
+
+TILE_GOOD = dict(x=X, tiles=TL, out=OUT, z=Z, sigma=0.5, B=1, T=2, Hg=68, Wg=120, C=48, tile=64, overlap=16)
+
+
+def _tg(**kw):
+    a = dict(TILE_GOOD)
+    a.update(kw)
+    return fastvr.tile_gather_raw(a["x"], a["tiles"], a["B"], a["T"], a["Hg"], a["Wg"], a["C"], a["tile"],
+                                  a["overlap"], None)
+
+
+def _tb(update=False, **kw):
+    a = dict(TILE_GOOD)
+    a.update(kw)
+    if update:
+        return fastvr.tile_blend_update_raw(a["tiles"], a["z"], a["out"], a["sigma"], a["B"], a["T"], a["Hg"], a["Wg"],
+                                            a["C"], a["tile"], a["overlap"], None)
+    return fastvr.tile_blend_raw(a["tiles"], a["out"], a["B"], a["T"], a["Hg"], a["Wg"], a["C"], a["tile"],
+                                 a["overlap"], None)
+
+
+def test_tile_axis_host_function(lib):
+    assert fastvr.tile_axis(68, 64, 16) == (2, 64)
+    assert fastvr.tile_axis(120, 64, 16) == (3, 64)
+    assert fastvr.tile_axis(30, 64, 16) == (1, 30)
+    with pytest.raises(fastvr.FastVRError):
+        fastvr.tile_axis(10, 4, 4)
+    with pytest.raises(fastvr.FastVRError):
+        fastvr.tile_axis(0, 4, 1)
+
+
+@pytest.mark.parametrize("fn,kw,status,needle", [
+    (_tg, dict(x=None), fastvr.ERR_INVALID_ARGUMENT, "x or tiles is NULL"),
+    (_tg, dict(tiles=TL + 8), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (_tg, dict(C=44), fastvr.ERR_INVALID_ARGUMENT, "multiple of 8"),
+    (_tg, dict(overlap=64), fastvr.ERR_INVALID_ARGUMENT, "overlap < tile"),
+    (_tg, dict(overlap=-1), fastvr.ERR_INVALID_ARGUMENT, "overlap < tile"),
+    (_tg, dict(tile=5000, overlap=0), fastvr.ERR_UNSUPPORTED, "tile"),
+    (_tg, dict(T=-1), fastvr.ERR_INVALID_ARGUMENT, "negative size"),
+    (_tg, dict(tiles=X + 1024), fastvr.ERR_INVALID_ARGUMENT, "tiles overlaps x"),
+    (_tb, dict(C=46), fastvr.ERR_INVALID_ARGUMENT, "multiple of 4"),
+    (_tb, dict(out=None), fastvr.ERR_INVALID_ARGUMENT, "tiles or out is NULL"),
+    (_tb, dict(out=TL + 64), fastvr.ERR_INVALID_ARGUMENT, "out overlaps tiles"),
+    (_tb, dict(Wg=1 << 27, C=64), fastvr.ERR_UNSUPPORTED, "2^31"),
+])
+def test_tile_rejects(lib, fn, kw, status, needle):
+    assert fn(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(z=None), "z_lq is NULL"),
+    (dict(z=Z + 4), "8-byte aligned"),
+    (dict(sigma=float("nan")), "sigma"),
+    (dict(out=Z + 16), "out overlaps z_lq"),
+])
+def test_tile_blend_update_rejects(lib, kw, needle):
+    assert _tb(update=True, **kw) == fastvr.ERR_INVALID_ARGUMENT
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(T=0), dict(Hg=0), dict(C=0)])
+def test_tile_empty_is_ok(lib, kw):
+    assert _tg(**kw) == fastvr.OK
+    assert _tb(**kw) == fastvr.OK
+    assert _tb(update=True, **kw) == fastvr.OK
 
 
 def test_error_is_thread_local(lib):
