@@ -65,55 +65,89 @@ __global__ __launch_bounds__(kThreads) void tile_gather_kernel(const u32x4* __re
   }
 }
 
-// One output row (b, t, y) per loop step of a workgroup; 4 channels (16 bytes of
-// fp32) per thread and step.  With Z (fused Eq. 9) the output is
+// One output row (b, t, y) per loop step of a workgroup.  A thread forms U
+// positions-times-4-channels units (16 bytes of fp32 each, kThreads apart) at a
+// time, issuing the loads of all U units from one tile before using any, so
+// several loads per thread are in flight.  With Z (fused Eq. 9) the output is
 // z - sigma * blend, z bf16.
+#ifndef FASTVR_BLEND_UNITS
+#define FASTVR_BLEND_UNITS 4
+#endif
 template <bool Z>
 __global__ __launch_bounds__(kThreads) void tile_blend_kernel(const float* __restrict__ tiles,
                                                               const uint16_t* __restrict__ z, float* __restrict__ out,
                                                               float neg_sigma, int T, int Hg, int Wg, int C, Axis ay,
                                                               Axis ax, int R, int64_t n_rows) {
+  constexpr int U = FASTVR_BLEND_UNITS;
   const int C4 = C / 4;
   const int row_units = Wg * C4;
   const int nt = ay.n * ax.n;
+  const int64_t tile_rows = (int64_t)T * ay.L;  // rows of one tile
   for (int64_t r = blockIdx.x; r < n_rows; r += gridDim.x) {
     // r = (b * T + t) * Hg + y  (wave-uniform)
     const int y = (int)(r % Hg);
     const int64_t bt = r / Hg;
     const int t = (int)(bt % T);
     const int64_t b = bt / T;
-    for (int u = threadIdx.x; u < row_units; u += kThreads) {
-      const int xg = u / C4, c4 = u - (u / C4) * C4;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      float wsum = 0.f;
+    for (int u0 = threadIdx.x; u0 < row_units; u0 += kThreads * U) {
+      int xg[U], c4[U];
+      bool ok[U];
+      f32x4 acc[U];
+      float wsum[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const int u = u0 + k * kThreads;
+        ok[k] = u < row_units;
+        xg[k] = ok[k] ? u / C4 : 0;
+        c4[k] = u - xg[k] * C4;
+        acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        wsum[k] = 0.f;
+      }
       for (int ty = 0; ty < ay.n; ++ty) {
         const int iy = y - origin(ay, ty);
         if (iy < 0 || iy >= ay.L) continue;
         const int wy = axis_weight(iy, ay.L, R);
+        const int64_t row0 = ((b * nt + ty * ax.n) * T + t) * ay.L + iy;  // tile row for tx = 0
         for (int tx = 0; tx < ax.n; ++tx) {
-          const int ix = xg - origin(ax, tx);
-          if (ix < 0 || ix >= ax.L) continue;
-          const float w = (float)(wy * axis_weight(ix, ax.L, R));
-          const int64_t tr = ((b * nt + ty * ax.n + tx) * T + t) * ay.L + iy;  // tile row
-          const f32x4 v = *reinterpret_cast<const f32x4*>(tiles + (tr * ax.L + ix) * C + 4 * c4);
-          acc.x = __builtin_fmaf(w, v.x, acc.x);
-          acc.y = __builtin_fmaf(w, v.y, acc.y);
-          acc.z = __builtin_fmaf(w, v.z, acc.z);
-          acc.w = __builtin_fmaf(w, v.w, acc.w);
-          wsum += w;
+          const int ox = origin(ax, tx);
+          const float* trow = tiles + (row0 + (int64_t)tx * tile_rows) * ax.L * C;
+          f32x4 val[U];
+          float w[U];
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            const int ix = xg[k] - ox;
+            val[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+            w[k] = 0.f;
+            if (ok[k] && ix >= 0 && ix < ax.L) {
+              w[k] = (float)(wy * axis_weight(ix, ax.L, R));
+              val[k] = *reinterpret_cast<const f32x4*>(trow + (int64_t)ix * C + 4 * c4[k]);
+            }
+          }
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            acc[k].x = __builtin_fmaf(w[k], val[k].x, acc[k].x);
+            acc[k].y = __builtin_fmaf(w[k], val[k].y, acc[k].y);
+            acc[k].z = __builtin_fmaf(w[k], val[k].z, acc[k].z);
+            acc[k].w = __builtin_fmaf(w[k], val[k].w, acc[k].w);
+            wsum[k] += w[k];
+          }
         }
       }
-      f32x4 res = {acc.x / wsum, acc.y / wsum, acc.z / wsum, acc.w / wsum};
-      const int64_t o = (r * Wg + xg) * C + 4 * c4;
-      if (Z) {
-        const uint64_t zz = *reinterpret_cast<const uint64_t*>(z + o);
-        const __bf16* zb = reinterpret_cast<const __bf16*>(&zz);
-        res.x = __builtin_fmaf(neg_sigma, res.x, (float)zb[0]);
-        res.y = __builtin_fmaf(neg_sigma, res.y, (float)zb[1]);
-        res.z = __builtin_fmaf(neg_sigma, res.z, (float)zb[2]);
-        res.w = __builtin_fmaf(neg_sigma, res.w, (float)zb[3]);
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if (!ok[k]) continue;
+        f32x4 res = {acc[k].x / wsum[k], acc[k].y / wsum[k], acc[k].z / wsum[k], acc[k].w / wsum[k]};
+        const int64_t o = (r * Wg + xg[k]) * C + 4 * c4[k];
+        if (Z) {
+          const uint64_t zz = *reinterpret_cast<const uint64_t*>(z + o);
+          const __bf16* zb = reinterpret_cast<const __bf16*>(&zz);
+          res.x = __builtin_fmaf(neg_sigma, res.x, (float)zb[0]);
+          res.y = __builtin_fmaf(neg_sigma, res.y, (float)zb[1]);
+          res.z = __builtin_fmaf(neg_sigma, res.z, (float)zb[2]);
+          res.w = __builtin_fmaf(neg_sigma, res.w, (float)zb[3]);
+        }
+        __builtin_nontemporal_store(res, reinterpret_cast<f32x4*>(out + o));
       }
-      __builtin_nontemporal_store(res, reinterpret_cast<f32x4*>(out + o));
     }
   }
 }
