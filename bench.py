@@ -79,9 +79,13 @@ def cpu_baseline(w, q, k, v, budget_rows: int, seed: int = 0):
         lo, hi = metrics.kv_interval(int(r) // w.chunk_len, w.n_tokens, w.chunk_len, w.window_chunks)
         vis += hi - lo
     flops = 4 * w.d * w.B * w.H * vis
+    total = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{budget_rows} seeded random query rows of the parallel 1080p call, all {w.H} heads, "
-                      f"{dt:.1f} s wall, fp64 NumPy/BLAS, host os.cpu_count()={os.cpu_count()}"}
+                      f"{dt:.1f} s wall, fp64 NumPy/BLAS ({threads} BLAS threads, 1 process), host "
+                      f"os.cpu_count()={os.cpu_count()}",
+            "wall_s_sample": round(dt, 2),
+            "wall_s_full_call_extrapolated": round(dt * total / flops, 1)}
 
 
 def _time_ms(torch, cur, fn, reps: int, warm: int = 2) -> float:
@@ -229,8 +233,8 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="1080p", choices=["1080p", "480p", "wide_sw", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=2560)
@@ -324,9 +328,12 @@ def main():
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
-    t_full = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+    per_full = sorted(e[0].elapsed_time(e[1]) for e in events)
+    per_str = sorted(e[2].elapsed_time(e[3]) for e in events) if stream else [0.0]
+    t_full = sum(per_full) / args.steps
     t_app = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps if stream else 0.0
-    t_str = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps if stream else 0.0
+    t_str = sum(per_str) / args.steps if stream else 0.0
+    med = lambda xs: xs[len(xs) // 2] if len(xs) % 2 else 0.5 * (xs[len(xs) // 2 - 1] + xs[len(xs) // 2])
     flops_step = f_full + f_stream
     value = flops_step / (ms_step * 1e-3) / 1e12
     n_launch = 2 if stream else 1
@@ -356,6 +363,8 @@ def main():
         },
         "ms_per_chunk": round(ms_step / n_chunks_per_step, 4),
         "calls_ms": {"full": round(t_full, 4), "kv_append": round(t_app, 4), "stream": round(t_str, 4)},
+        "calls_ms_median": {"full": round(med(per_full), 4), "stream": round(med(per_str), 4)},
+        "calls_ms_min": {"full": round(per_full[0], 4), "stream": round(per_str[0], 4)},
         "calls_tflops": {"full": round(f_full / (t_full * 1e-3) / 1e12, 2),
                          "stream": round(f_stream / (t_str * 1e-3) / 1e12, 2) if stream else None},
         "effective_flop_per_step": flops_step,

@@ -1,8 +1,10 @@
 """Parity at the full sizes of the benchmark workloads, in the launch
-configuration the benchmark times.  The oracle evaluates a stratified sample
-of query rows (every chunk and 256-row tile boundary, the ragged tail, and
-seeded random rows); the streaming step is also checked bit for bit against
-the parallel call over the whole sequence."""
+configuration the benchmark times.  Coverage per workload: tiny and 480p every
+row of every head; 1080p and the wide sliding window a stratified sample of
+query rows, evaluated for every head (every chunk and 256-row tile boundary,
+the ragged tail, and 4096 / 2048 seeded random rows); the 1080p streaming step
+bit for bit against the parallel call over every row and head, and every one of
+its 16320 rows against the oracle for two heads."""
 import numpy as np
 import pytest
 import torch
@@ -52,13 +54,13 @@ def test_tiny_all_rows(dev):
     compare(to_np(o), to_np(lse), o_ref, l_ref, label="tiny (all rows)")
 
 
-def test_480p_sampled(dev):
+def test_480p_all_rows(dev):
     w = WORKLOADS["480p"]
-    _announce("480p B=1 H=12 d=128 N=18720 L=3120")
+    _announce("480p B=1 H=12 d=128 N=18720 L=3120 (all rows)")
     q, k, v = make_sequence(w)
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
-    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=1024, seed=2)
-    _check_rows(w, q, k, v, o, lse, rows, "480p")
+    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
+    compare(to_np(o), to_np(lse), o_ref, l_ref, label="480p (all rows)")
 
 
 def test_1080p_full_and_streaming_step(dev):
@@ -67,7 +69,7 @@ def test_1080p_full_and_streaming_step(dev):
     _announce("1080p B=1 H=12 d=128 N=65280 L=16320 + streaming step chunk 3")
     q, k, v = make_sequence(w)
     qd, kd, vd, o, lse = _full_call(w, q, k, v, dev)
-    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=256, seed=3, band=0)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=4096, seed=3, band=0)
     _check_rows(w, q, k, v, o, lse, rows, "1080p")
 
     # streaming step: cache holds chunks 0-2, append chunk 3, attend chunk 3
@@ -86,9 +88,13 @@ def test_1080p_full_and_streaming_step(dev):
     assert torch.equal(kc, kd) and torch.equal(vc, vd)
     assert torch.equal(so, o[:, lo:lo + so.shape[1]]), "streaming step differs from the parallel call"
     assert torch.equal(sl, lse[:, :, lo:lo + so.shape[1]])
-    srows = sample_rows(so.shape[1], ws.chunk_len, n_random=128, seed=4, band=0)
-    _check_rows(ws, q[:, lo:lo + so.shape[1]], k, v, so, sl, srows, "1080p streaming step",
-                q_chunk_offset=sv["q_chunk_offset"])
+    # every row of the streaming step, two heads
+    heads = [0, 7]
+    hs = torch.as_tensor(heads, device=so.device)
+    o_ref, l_ref = run_oracle(q[:, lo:lo + so.shape[1], heads], k[:, :, heads], v[:, :, heads], ws.chunk_len,
+                              sv["q_chunk_offset"], ws.window_chunks, ws.scale)
+    compare(to_np(so[:, :, hs]), to_np(sl[:, hs]), o_ref, l_ref,
+            label=f"1080p streaming step (all {so.shape[1]} rows, heads {heads})")
 
 
 def test_wide_sliding_window_sampled(dev):
@@ -96,5 +102,5 @@ def test_wide_sliding_window_sampled(dev):
     _announce("wide_sw B=1 H=24 d=128 N=138720 L=16320 W=2 outliers")
     q, k, v = make_sequence(w)
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
-    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=128, seed=5, band=0, tile=1024)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=2048, seed=5, band=0, tile=1024)
     _check_rows(w, q, k, v, o, lse, rows, "wide_sw")
