@@ -75,12 +75,6 @@ constexpr int kStages = 3;                // LDS buffers per operand
 #ifndef FASTVR_DMA_SPLIT
 #define FASTVR_DMA_SPLIT 1
 #endif
-//  FASTVR_MAX_SLACK  > 0: the running maximum moves only when a row's maximum
-//                    exceeds it by more than this (log2 units), so P <= 2^slack
-//                    and O is rescaled only on such jumps; 0: exact running maximum
-#ifndef FASTVR_MAX_SLACK
-#define FASTVR_MAX_SLACK 0
-#endif
 static_assert(kBQ == kFwdRowsPerItem, "tile height mismatch");
 
 struct Params {
@@ -383,15 +377,8 @@ struct Attn {
     float other;
     const float mine = swap_halves(mx, &other);
     mx = NEG ? __builtin_fminf(mine, other) : __builtin_fmaxf(mine, other);
-#if FASTVR_MAX_SLACK > 0
-    const float cand = mx * c;
-    const bool grow = cand > m_run + (float)FASTVR_MAX_SLACK;  // always on the first tile (m_run = -inf)
-    const float m_new = grow ? cand : m_run;
-    alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-#else
     const float m_new = __builtin_fmaxf(m_run, mx * c);
     alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
-#endif
     m_run = m_new;
     const float nm = -m_new;
 #pragma unroll
