@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 5
+#define FASTVR_ABI_VERSION 6
 
 typedef enum {
   FASTVR_OK = 0,
@@ -78,16 +78,19 @@ fastvr_status fastvr_chunk_attn_fwd(const void* q, const void* k, const void* v,
 
 /*
  * Same operation with explicit element strides, for tensors that are views
- * (e.g. a KV cache [B, capacity, H, d] with capacity > Nkv and B > 1).
- * Within a token, heads are contiguous with stride d and head_dim elements are
- * contiguous.  Strides are in elements: *_sb between batches, *_st between
- * tokens.  The bf16 strides must be multiples of 8 and the fp32 ones of 4
- * (16-byte rows), and each must be >= H * d.  lse is [B, H, Nq] contiguous.
+ * (e.g. a KV cache [B, capacity, H, d] with capacity > Nkv and B > 1), and a
+ * choice of output type: o_bf16 = 0 stores O as fp32, o_bf16 = 1 as bf16 (the
+ * fp32 value rounded to nearest even).  Within a token, heads are contiguous
+ * with stride d and head_dim elements are contiguous.  Strides are in elements:
+ * *_sb between batches, *_st between tokens.  The bf16 strides must be
+ * multiples of 8 and the fp32 ones of 4 (16-byte rows), and each must be
+ * >= H * d.  lse is [B, H, Nq] contiguous.  o_bf16 not in {0, 1}:
+ * FASTVR_ERR_INVALID_ARGUMENT.
  */
 fastvr_status fastvr_chunk_attn_fwd_ex(const void* q, int64_t q_sb, int64_t q_st,
                                        const void* k, int64_t k_sb, int64_t k_st,
                                        const void* v, int64_t v_sb, int64_t v_st,
-                                       float* o, int64_t o_sb, int64_t o_st, float* lse,
+                                       void* o, int64_t o_sb, int64_t o_st, int32_t o_bf16, float* lse,
                                        int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
                                        int64_t chunk_len, int64_t q_chunk_offset,
                                        int64_t window_chunks, float scale, void* stream);

@@ -81,13 +81,14 @@ struct Params {
   const uint16_t* q;
   const uint16_t* k;
   const uint16_t* v;
-  float* o;
+  void* o;        // fp32, or bf16 when o_bf16
   float* lse;
   int64_t q_sb, k_sb, v_sb, o_sb;  // batch strides (elements)
   int32_t q_st, k_st, v_st, o_st;  // token strides (elements, < 2^22)
   int32_t nq, nkv, chunk_len, q_chunk_offset, window;  // window -1 = unbounded
   int32_t B, H, n_local_chunks, tiles_full, tiles_last, n_items;
   float c;  // scale * log2(e)
+  int32_t o_bf16;  // 1: O stored as bf16 (round to nearest even), 0: fp32
   // Bounded ring cache (ring step only): key rows are virtual rows over the
   // visible chunks in chunk order; chunk s < n_seg - 1 is read from ring slot
   // (ring_first + s) mod ring_slots, the last (new) one from k / v above.
@@ -705,7 +706,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   const float l_tot = l_mine + l_other;
   if (row < q_end) {
     const float inv = 1.0f / l_tot;
-    float* ob = p.o + (int64_t)b * p.o_sb + (int64_t)row * p.o_st + (int64_t)h * D;
+    const int64_t oo = (int64_t)b * p.o_sb + (int64_t)row * p.o_st + (int64_t)h * D;
 #pragma unroll
     for (int dm = 0; dm < D / 32; ++dm)
 #pragma unroll
@@ -715,7 +716,14 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
         val.y = a.o[dm][4 * g + 1] * inv;
         val.z = a.o[dm][4 * g + 2] * inv;
         val.w = a.o[dm][4 * g + 3] * inv;
-        *reinterpret_cast<f32x4*>(ob + dm * 32 + g * 8 + a.hh * 4) = val;
+        const int64_t e = oo + dm * 32 + g * 8 + a.hh * 4;
+        if (p.o_bf16) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          const bf16x4 r = {(__bf16)val.x, (__bf16)val.y, (__bf16)val.z, (__bf16)val.w};
+          *reinterpret_cast<bf16x4*>(static_cast<uint16_t*>(p.o) + e) = r;
+        } else {
+          *reinterpret_cast<f32x4*>(static_cast<float*>(p.o) + e) = val;
+        }
       }
     if (a.hh == 0 && p.lse != nullptr)
       p.lse[((int64_t)b * p.H + h) * p.nq + row] = (a.m_run + __builtin_log2f(l_tot)) * kLn2;
@@ -753,6 +761,7 @@ hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   p.k = static_cast<const uint16_t*>(a.k);
   p.v = static_cast<const uint16_t*>(a.v);
   p.o = a.o;
+  p.o_bf16 = a.o_bf16 ? 1 : 0;
   p.lse = a.lse;
   // Validated by the caller: sizes < 2^31, token strides < 2^22.  A chunk longer
   // than the key range (only possible with q_chunk_offset = 0) is the same as a

@@ -95,7 +95,8 @@ struct Ring {
 };
 
 fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k, int64_t k_sb, int64_t k_st,
-                       const void* v, int64_t v_sb, int64_t v_st, float* o, int64_t o_sb, int64_t o_st, float* lse,
+                       const void* v, int64_t v_sb, int64_t v_st, void* o, int64_t o_sb, int64_t o_st, int o_bf16,
+                       float* lse,
                        int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
                        int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream,
                        const Ring& ring = Ring()) {
@@ -129,7 +130,9 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
   const int64_t kv_rows = ring.k != nullptr ? Nq : Nkv;
   if ((s = check_view({"k", k, k_sb, k_st, kv_rows, 2}, B, hd, &kb)) != FASTVR_OK) return s;
   if ((s = check_view({"v", v, v_sb, v_st, kv_rows, 2}, B, hd, &vb)) != FASTVR_OK) return s;
-  if ((s = check_view({"o", o, o_sb, o_st, Nq, 4}, B, hd, &ob)) != FASTVR_OK) return s;
+  if (o_bf16 != 0 && o_bf16 != 1)
+    return fail(FASTVR_ERR_INVALID_ARGUMENT, "o_bf16 must be 0 or 1 (got %d)", o_bf16);
+  if ((s = check_view({"o", o, o_sb, o_st, Nq, o_bf16 ? 2 : 4}, B, hd, &ob)) != FASTVR_OK) return s;
   if (q_st >= fastvr::kMaxTokenStride || k_st >= fastvr::kMaxTokenStride || v_st >= fastvr::kMaxTokenStride ||
       o_st >= fastvr::kMaxTokenStride)
     return fail(FASTVR_ERR_UNSUPPORTED, "token strides must be below %lld elements",
@@ -162,6 +165,7 @@ fastvr_status fwd_impl(const void* q, int64_t q_sb, int64_t q_st, const void* k,
 
   fastvr::FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
+  a.o_bf16 = o_bf16 == 1;
   a.q_sb = q_sb; a.q_st = q_st;
   a.k_sb = k_sb; a.k_st = k_st;
   a.v_sb = v_sb; a.v_st = v_st;
@@ -194,17 +198,17 @@ fastvr_status fastvr_chunk_attn_fwd(const void* q, const void* k, const void* v,
   if (H >= 0 && d >= 0 && Nq >= 0 && Nkv >= 0 &&
       (!mul_ok(H, d, &hd) || !mul_ok(Nq, hd, &sq) || !mul_ok(Nkv, hd, &skv)))
     return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
-  return fwd_impl(q, sq, hd, k, skv, hd, v, skv, hd, o, sq, hd, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+  return fwd_impl(q, sq, hd, k, skv, hd, v, skv, hd, o, sq, hd, 0, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
                   window_chunks, scale, stream);
 }
 
 fastvr_status fastvr_chunk_attn_fwd_ex(const void* q, int64_t q_sb, int64_t q_st, const void* k, int64_t k_sb,
-                                       int64_t k_st, const void* v, int64_t v_sb, int64_t v_st, float* o,
-                                       int64_t o_sb, int64_t o_st, float* lse, int64_t B, int64_t H, int64_t Nq,
-                                       int64_t Nkv, int64_t d, int64_t chunk_len, int64_t q_chunk_offset,
+                                       int64_t k_st, const void* v, int64_t v_sb, int64_t v_st, void* o,
+                                       int64_t o_sb, int64_t o_st, int32_t o_bf16, float* lse, int64_t B, int64_t H,
+                                       int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len, int64_t q_chunk_offset,
                                        int64_t window_chunks, float scale, void* stream) {
-  return fwd_impl(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, B, H, Nq, Nkv, d, chunk_len,
-                  q_chunk_offset, window_chunks, scale, stream);
+  return fwd_impl(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, o_bf16, lse, B, H, Nq, Nkv, d,
+                  chunk_len, q_chunk_offset, window_chunks, scale, stream);
 }
 
 fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, const void* v_new, void* k_ring,
@@ -252,7 +256,7 @@ fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, 
   // queries: the new chunk, which is chunk n_prev of the visible sequence; keys:
   // the visible chunks, virtual rows 0 .. nkv - 1 (the kernel reads the earlier
   // ones from the ring and the new one from k_new / v_new)
-  return fwd_impl(q_new, sn, hd, k_new, sn, hd, v_new, sn, hd, o, sn, hd, lse, B, H, n_new, nkv, d, chunk_len,
+  return fwd_impl(q_new, sn, hd, k_new, sn, hd, v_new, sn, hd, o, sn, hd, 0, lse, B, H, n_new, nkv, d, chunk_len,
                   n_prev, window_chunks, scale, stream, r);
 }
 

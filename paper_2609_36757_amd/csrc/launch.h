@@ -11,7 +11,7 @@ struct FwdArgs {
   const void* q;
   const void* k;
   const void* v;
-  float* o;
+  void* o;               // fp32, or bf16 when o_bf16
   float* lse;            // may be null
   int64_t q_sb, q_st;    // element strides: batch, token (bf16)
   int64_t k_sb, k_st;
@@ -20,6 +20,7 @@ struct FwdArgs {
   int64_t B, H, nq, nkv, d;
   int64_t chunk_len, q_chunk_offset, window_chunks;
   float scale;
+  bool o_bf16 = false;
   // Ring step (k_ring != nullptr): k / v are the new chunk, the earlier visible
   // chunks come from the ring; the kernel also writes k / v into new_slot.
   void* k_ring = nullptr;

@@ -47,7 +47,7 @@ def load() -> ctypes.CDLL:
                                           _i64, ctypes.c_float, _vp]
     lib.fastvr_chunk_attn_fwd_ex.restype = ctypes.c_int
     lib.fastvr_chunk_attn_fwd_ex.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64,
-                                             _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
+                                             ctypes.c_int32, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _i64, _i64,
                                              ctypes.c_float, _vp]
     lib.fastvr_kv_cache_append.restype = ctypes.c_int
     lib.fastvr_kv_cache_append.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, _vp]
@@ -100,10 +100,10 @@ def fwd_raw(q, k, v, o, lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window
                                         window_chunks, scale, stream)
 
 
-def fwd_ex_raw(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse, B, H, Nq, Nkv, d,
+def fwd_ex_raw(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, o_bf16, lse, B, H, Nq, Nkv, d,
                chunk_len, q_chunk_offset, window_chunks, scale, stream=0) -> int:
-    return load().fastvr_chunk_attn_fwd_ex(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, lse,
-                                           B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks,
+    return load().fastvr_chunk_attn_fwd_ex(q, q_sb, q_st, k, k_sb, k_st, v, v_sb, v_st, o, o_sb, o_st, o_bf16,
+                                           lse, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks,
                                            scale, stream)
 
 
@@ -171,9 +171,10 @@ def chunk_attn(q, k, v, *, chunk_len: int, q_chunk_offset: int = 0, window_chunk
                scale: float | None = None, out=None, lse=None, return_lse: bool = True, stream=None):
     """Chunk-causal attention forward (FastVR Sec. 3.1, Eq. 1).
 
-    q [B, Nq, H, d], k/v [B, Nkv, H, d] bf16 CUDA tensors (views allowed when
-    heads and head_dim are packed).  Returns (o fp32 [B, Nq, H, d], lse fp32
-    [B, H, Nq] or None)."""
+    q [B, Nq, H, d], k/v [B, Nkv, H, d] bf16 GPU tensors (views allowed when
+    heads and head_dim are packed).  Returns (o [B, Nq, H, d], lse fp32
+    [B, H, Nq] or None); o is fp32 unless ``out`` is a bfloat16 tensor, which
+    receives O rounded to bf16."""
     import torch
     for name, t in (("q", q), ("k", k), ("v", v)):
         if t.dtype != torch.bfloat16 or not t.is_cuda:
@@ -186,8 +187,9 @@ def chunk_attn(q, k, v, *, chunk_len: int, q_chunk_offset: int = 0, window_chunk
         scale = 1.0 / math.sqrt(d)
     if out is None:
         out = torch.empty((B, Nq, H, d), dtype=torch.float32, device=q.device)
-    if out.dtype != torch.float32 or tuple(out.shape) != (B, Nq, H, d):
-        raise ValueError("out must be float32 [B, Nq, H, d]")
+    if out.dtype not in (torch.float32, torch.bfloat16) or tuple(out.shape) != (B, Nq, H, d):
+        raise ValueError("out must be float32 or bfloat16 [B, Nq, H, d]")
+    o_bf16 = 1 if out.dtype == torch.bfloat16 else 0
     if return_lse and lse is None:
         lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (B, H, Nq)
@@ -195,12 +197,12 @@ def chunk_attn(q, k, v, *, chunk_len: int, q_chunk_offset: int = 0, window_chunk
         raise ValueError("lse must be a contiguous float32 [B, H, Nq] tensor")
     lse_ptr = lse.data_ptr() if lse is not None else None
     st = _stream_handle(stream)
-    if all(t.is_contiguous() for t in (q, k, v, out)):
+    if not o_bf16 and all(t.is_contiguous() for t in (q, k, v, out)):
         status = fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse_ptr, B, H, Nq, Nkv, d,
                          chunk_len, q_chunk_offset, window_chunks, scale, st)
     else:
         qs, ks, vs, os_ = (_bnhd_strides(t, n) for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out")))
-        status = fwd_ex_raw(q.data_ptr(), *qs, k.data_ptr(), *ks, v.data_ptr(), *vs, out.data_ptr(), *os_,
+        status = fwd_ex_raw(q.data_ptr(), *qs, k.data_ptr(), *ks, v.data_ptr(), *vs, out.data_ptr(), *os_, o_bf16,
                             lse_ptr, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks, scale, st)
     _check(status)
     return out, lse

@@ -40,7 +40,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 5
+    assert lib.fastvr_abi_version() == 6
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -104,11 +104,12 @@ def test_fwd_empty_problem_is_ok(lib, kw):
 
 def _fwd_ex(**kw):
     a = dict(GOOD, B=2, q_sb=64 * 128, q_st=128, k_sb=64 * 128, k_st=128, v_sb=64 * 128, v_st=128,
-             o_sb=64 * 128, o_st=128)
+             o_sb=64 * 128, o_st=128, o_bf16=0)
     a.update(kw)
     return fastvr.fwd_ex_raw(a["q"], a["q_sb"], a["q_st"], a["k"], a["k_sb"], a["k_st"], a["v"], a["v_sb"],
-                             a["v_st"], a["o"], a["o_sb"], a["o_st"], a["lse"], a["B"], a["H"], a["Nq"], a["Nkv"],
-                             a["d"], a["chunk_len"], a["q_chunk_offset"], a["window_chunks"], a["scale"], None)
+                             a["v_st"], a["o"], a["o_sb"], a["o_st"], a["o_bf16"], a["lse"], a["B"], a["H"],
+                             a["Nq"], a["Nkv"], a["d"], a["chunk_len"], a["q_chunk_offset"], a["window_chunks"],
+                             a["scale"], None)
 
 
 @pytest.mark.parametrize("kw,needle", [
@@ -118,6 +119,9 @@ def _fwd_ex(**kw):
     (dict(v_sb=100 * 128 + 4), "multiples of 8"),
     (dict(o_sb=63 * 128), "batch stride"),
     (dict(k_sb=BIG, k_st=BIG // 4), "overflows"),
+    (dict(o_bf16=2), "o_bf16 must be 0 or 1"),
+    (dict(o_bf16=1, o_st=132), "multiples of 8"),       # bf16 O rows: 16-byte strides are multiples of 8
+    (dict(o_bf16=1, o=O + 8), "aligned"),
 ])
 def test_fwd_ex_rejects_bad_strides(lib, kw, needle):
     assert _fwd_ex(**kw) == fastvr.ERR_INVALID_ARGUMENT

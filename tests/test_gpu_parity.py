@@ -173,3 +173,25 @@ def test_streaming_with_cache_equals_parallel(dev, W):
             assert torch.equal(cl_, full_l[:, :, s]), f"compacted chunk {c}"
     o_ref, l_ref = run_oracle(q.cpu(), k.cpu(), v.cpu(), L, 0, W, default_scale(d))
     compare(to_np(full_o), to_np(full_l), o_ref, l_ref, label=f"streaming W={W}")
+
+
+@pytest.mark.parametrize("strided", [False, True])
+def test_bf16_output_is_the_rounded_fp32_output(dev, strided):
+    """fastvr_chunk_attn_fwd_ex with o_bf16 = 1 stores the fp32 result rounded to
+    bf16 (nearest even), bit for bit, also into a strided view, and the LSE is
+    unchanged."""
+    B, H, d, N, L = 2, 3, 128, 500, 120
+    print(f"\n[gpu case] bf16 O strided={strided} B={B} H={H} d={d} N={N} L={L}", flush=True)
+    q, k, v = (t.to(dev) for t in make_qkv(B, N, N, H, d, seed=44))
+    o32, l32 = fastvr.chunk_attn(q, k, v, chunk_len=L, window_chunks=1)
+    if strided:
+        big = torch.full((B, N + 17, H, d), float("nan"), dtype=torch.bfloat16, device=dev)
+        ob = big[:, 5:5 + N]
+    else:
+        ob = torch.empty((B, N, H, d), dtype=torch.bfloat16, device=dev)
+    _, l16 = fastvr.chunk_attn(q, k, v, chunk_len=L, window_chunks=1, out=ob)
+    torch.cuda.synchronize()
+    assert torch.equal(ob.view(torch.int16), o32.to(torch.bfloat16).view(torch.int16))
+    assert torch.equal(l16, l32)
+    if strided:
+        assert torch.isnan(big[:, :5].float()).all() and torch.isnan(big[:, 5 + N:].float()).all()
