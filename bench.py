@@ -12,8 +12,9 @@ value = effective (unmasked) TFLOP/s of the whole step: 4 * d * visible pairs
 After the timed steps (and outside them) it reports ms/call and TFLOP/s of
 the 480p-shaped and wide sliding-window calls, of the W = 1 ring-cache
 streaming step, of the backward of the 1080p call, of the one-step latent
-update and of tiled inference with overlapping 64 x 64 latent tiles
-(``other_workloads``), then the fp64 oracle baseline.
+update, of tiled inference with overlapping 64 x 64 latent tiles and of the
+parallel calls with cold caches (``other_workloads``), then the fp64 oracle
+baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
 """
@@ -187,6 +188,40 @@ def tiled_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w):
             "blend_update_GB/s": gb(vt.numel() * 4 + z.numel() * 2 + zh.numel() * 4, ms_u)}
 
 
+def cold_cache(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080, reps: int = 5):
+    """The 1080p and 480p parallel calls with the caches flushed before every call:
+    a 512 MB buffer (twice the Infinity Cache) is overwritten between calls, and
+    only the attention call itself is timed (HIP events around each call)."""
+    from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    res = {}
+    for name in ("1080p", "480p"):
+        w = WORKLOADS[name]
+        if name == "1080p":
+            q, k, v = qd, kd, vd
+        else:
+            q, k, v = (t.to(dev) for t in make_sequence(w))
+        o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
+        lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
+        call = lambda: fastvr.chunk_attn(q, k, v, chunk_len=w.chunk_len, window_chunks=w.window_chunks,
+                                         scale=w.scale, out=o, lse=lse)
+        call()
+        times = []
+        for _ in range(reps):
+            flush.fill_(1)
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record(cur)
+            call()
+            e.record(cur)
+            torch.cuda.synchronize()
+            times.append(s.elapsed_time(e))
+        ms = sorted(times)[len(times) // 2]
+        f = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
+        res[name] = {"ms_median": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 2)}
+    del flush
+    return res
+
+
 def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     """ms/call and effective TFLOP/s of the other synthetic workloads: the
     480p-shaped and the wide sliding-window parallel calls, and the paper's
@@ -227,6 +262,7 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     res["bwd_1080p"] = backward_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w, 5)
     res.update(one_step_update_timing(torch, fastvr, dev, cur))
     res["tiled_1080p"] = tiled_1080p(torch, fastvr, metrics, dev, cur, qd, kd, vd, w)
+    res["cold_cache"] = cold_cache(torch, fastvr, metrics, dev, cur, qd, kd, vd, w)
     return res
 
 
