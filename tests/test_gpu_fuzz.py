@@ -61,7 +61,14 @@ def test_fuzz_forward_and_backward(dev, i):
     for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), refs):
         g64 = to_np(got)
         assert np.isfinite(g64).all(), (i, name)
-        rel = float(np.linalg.norm(g64 - ref) / max(np.linalg.norm(ref), 1e-30))
-        print(f"[parity] fuzz {i} {name} rel_fro={rel:.3e}", flush=True)
+        err = float(np.abs(g64 - ref).max())
+        if np.linalg.norm(ref) < 1e-6:
+            # an exactly vanishing gradient (e.g. a single visible key: dS = 0):
+            # the GPU keeps only fp32 rounding noise of dP - D
+            print(f"[parity] fuzz {i} {name} reference ~ 0, max_abs={err:.3e}", flush=True)
+            assert err <= 1e-4, (i, name, err)
+            continue
+        rel = float(np.linalg.norm(g64 - ref) / np.linalg.norm(ref))
+        print(f"[parity] fuzz {i} {name} rel_fro={rel:.3e} max_abs={err:.3e}", flush=True)
         # bf16 rounding of P and dS: expected about u / sqrt(3) = 2.3e-3 (see test_gpu_bwd.py)
-        assert rel <= 1e-2 or np.linalg.norm(ref) < 1e-6, (i, name, rel)
+        assert rel <= 1e-2, (i, name, rel)
