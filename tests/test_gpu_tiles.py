@@ -35,6 +35,9 @@ GEOMS = [
     (1, 1, 40, 33, 8, 16, 5),
     (1, 2, 9, 9, 24, 4, 3),        # heavy overlap: positions covered by several tiles
     (1, 1, 24, 36, 8, 12, 0),      # disjoint tiles
+    (1, 1, 20, 70, 1536, 64, 16),  # attention-output width: a blend segment spans under 3 positions
+    (1, 1, 1, 65537, 8, 2, 1),     # 65536 tiles along x: n * size > 2^32, the blend's 64-bit index path
+    (1, 300, 300, 4, 8, 64, 16),   # 90000 output rows: more rows than blend workgroups along y
 ]
 
 
