@@ -223,12 +223,12 @@ def cold_cache(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080, reps: int = 
 
 
 def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
-    """ms/call and effective TFLOP/s of the other synthetic workloads: the
-    480p-shaped and the wide sliding-window parallel calls, and the paper's
-    W = 1 streaming step with the bounded ring cache at the 1080p chunk shape."""
+    """ms/call and effective TFLOP/s of the other synthetic workloads: the tiny,
+    480p-shaped and wide sliding-window parallel calls, and the paper's W = 1
+    streaming step with the bounded ring cache at the 1080p chunk shape."""
     from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence
     res = {}
-    for name, reps in (("480p", 20), ("wide_sw", 3)):
+    for name, reps in (("tiny", 50), ("480p", 20), ("wide_sw", 3)):
         w = WORKLOADS[name]
         q, k, v = (t.to(dev) for t in make_sequence(w))
         o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
