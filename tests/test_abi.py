@@ -385,3 +385,23 @@ def test_workload_registry_shapes():
     assert (w["wide_sw"].n_tokens, w["wide_sw"].window_chunks, w["wide_sw"].n_chunks) == (138720, 2, 9)
     assert w["1080p_stream"].stream_chunk == 3 and w["1080p_stream"].seed == w["1080p"].seed
     assert w["tiny"].d == 64 and w["tiny"].scale == 0.125
+
+
+def test_c_client_compiles_and_runs(lib, tmp_path):
+    """The header compiles as strict C99 and a C program linked against the
+    library gets the same host-side results (tests/c_abi_client.c)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    here = os.path.dirname(os.path.abspath(__file__))
+    libdir = os.path.dirname(fastvr.LIB_PATH)
+    exe = str(tmp_path / "c_abi_client")
+    cmd = [cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", os.path.dirname(HEADER),
+           os.path.join(here, "c_abi_client.c"), "-o", exe, f"-L{libdir}", "-lfastvr", f"-Wl,-rpath,{libdir}",
+           "-Wl,--allow-shlib-undefined"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
