@@ -18,8 +18,8 @@
 // Matrix-core / vector-ALU ping-pong: waves 0-3 (group A) and 4-7 (group B)
 // share the four SIMDs one-to-one.  Time is cut into slots separated by
 // workgroup barriers, and the two groups swap roles every slot:
-//  * matrix-core slot: the 16 QK MFMAs of tile j, then the 16 P.V MFMAs of tile
-//    j-1 with the row statistics of the new scores (running maximum, rescale
+//  * matrix-core slot: the QK MFMAs of key tile j (24 for 96 keys and d = 128),
+//    then the P.V MFMAs of tile j-1 (as many) with the row statistics of the new scores (running maximum, rescale
 //    factor, s * c - m) issued between them, so that this wave's vector-ALU
 //    work hides under its own matrix-core time;
 //  * vector-ALU slot: exp2, row sums, bf16 rounding of P and the rescale of O,
@@ -27,7 +27,7 @@
 // Each SIMD therefore always has a matrix-core wave and a vector-ALU wave side
 // by side.
 //
-// Memory: all K and V tiles (64 keys) travel by DMA straight from HBM into LDS
+// Memory: all K and V tiles (96 keys) travel by DMA straight from HBM into LDS
 // (buffer_load ... lds, per-tile buffer descriptors: rows outside the visible
 // interval read as zero), triple-buffered and issued two tiles ahead, K in the
 // even slots and V in the odd ones.  Both tiles are stored row-major, K with
@@ -52,7 +52,16 @@ using namespace dev;
 
 constexpr int kWaves = kFwdThreads / 64;  // 8
 constexpr int kBQ = 32 * kWaves;          // 256 query rows per workgroup
-constexpr int kBK = 64;                   // keys per KV tile
+#ifndef FASTVR_BK
+#define FASTVR_BK 96
+#endif
+constexpr int kBK = FASTVR_BK;            // keys per KV tile (FASTVR_BK: 64 or 96)
+constexpr int kKB = kBK / 32;             // 32-key blocks of a tile (score accumulators)
+constexpr int kKG = kBK / 16;             // 16-key groups of a tile (P fragments)
+// 96 keys: 48 MFMAs per matrix-core slot instead of 32 spread each slot's fixed
+// costs (operand-read ramp, barrier skew) over more work; three stages of K and
+// V then take 144 KB of LDS (d = 128), so 128 keys would not fit
+static_assert(kBK == 64 || kBK == 96, "key tile of 64 or 96 keys");
 constexpr int kStages = 3;                // LDS buffers per operand
 // Tuning switches (compile time):
 //  FASTVR_SCHED      order MFMAs, LDS reads and vector-ALU work with scheduling groups
@@ -150,6 +159,7 @@ struct Attn {
   static constexpr int kDmaPer = kBK * kChunks / (64 * kDmaWaves);  // DMA instructions per issuing wave per tile
   static constexpr int kLdsElems = 2 * kStages * kStage;
   static_assert(kDmaPer >= 1 && kChunks >= 8, "head_dim must be 64 or 128");
+  static_assert((kBK * kChunks) % (64 * kDmaWaves) == 0, "a tile is a whole number of DMA instructions per wave");
 
   int lane, wave, n, hh;
   int lo, hi, n_tiles;
@@ -168,8 +178,8 @@ struct Attn {
   int v_rd[D / 32];                // byte offsets of this lane's V^T transpose reads
   u32x4 qf[D / 16];
   f32x16 o[D / 32];
-  f32x16 s[2];
-  u32x4 pf[4];
+  f32x16 s[kKB];
+  u32x4 pf[kKG];
   float m_run, l_run;
   float alpha;  // rescale factor of the tile whose statistics were taken last
 
@@ -315,7 +325,7 @@ struct Attn {
     }
   }
 
-  // DMA of K (or V) tile j (64 keys from lo + 64 j) into LDS stage `stage`
+  // DMA of K (or V) tile j (kBK keys from lo + kBK j) into LDS stage `stage`
   __device__ __forceinline__ void load_k(int j, int stage) {
     if (RING) {
       load_ring<true>(j, stage);
@@ -337,7 +347,7 @@ struct Attn {
   }
 
   __device__ __forceinline__ u32x4 read_k(const char* kst, int i) const {
-    const int kk = i >> 1, mb = i & 1;
+    const int kk = i / kKB, mb = i % kKB;
     return *reinterpret_cast<const u32x4*>(kst + k_rd[kk] + mb * 32 * (D * 2));
   }
 
@@ -362,7 +372,7 @@ struct Attn {
     if (MASK) asm volatile("" : "+v"(lim));
     float part[4] = {NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf};
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kKB; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float x = s[mb][v];
@@ -383,7 +393,7 @@ struct Attn {
     m_run = m_new;
     const float nm = -m_new;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kKB; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float t = __builtin_fmaf(s[mb][v], c, nm);
@@ -399,17 +409,17 @@ struct Attn {
   // to bf16 fragments, l = l * alpha + rowsum(P), O *= alpha.
   __device__ __forceinline__ void softmax_rest() {
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kKB; ++mb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(s[mb][v]);
     float ps[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kKB; ++mb)
 #pragma unroll
       for (int v = (mb == 0 ? 4 : 0); v < 16; ++v) ps[v & 3] += s[mb][v];
     l_run = l_run * alpha + ((ps[0] + ps[1]) + (ps[2] + ps[3]));
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
+    for (int g = 0; g < kKG; ++g) {
       bf16x8 b;
 #pragma unroll
       for (int r = 0; r < 8; ++r) b[r] = (__bf16)s[g >> 1][8 * (g & 1) + r];
@@ -430,7 +440,7 @@ struct Attn {
   // two transpose reads of 4 keys each.
   template <bool QK, bool PV, bool STATS>
   __device__ __forceinline__ void mfma_slot(int st_k, int st_v) {
-    constexpr int kN = D / 8;  // MFMAs of each kind (QK: D/16 x 2 key blocks; PV: 4 key groups x D/32)
+    constexpr int kN = D * kBK / 512;  // MFMAs of each kind (QK: D/16 x kKB key blocks; PV: kKG key groups x D/32)
     constexpr int kAhead = FASTVR_AHEAD < kN ? FASTVR_AHEAD : kN;
 #if FASTVR_PRIO
     __builtin_amdgcn_s_setprio(1);
@@ -448,7 +458,7 @@ struct Attn {
           kf[i + kAhead] = read_k(kst, i + kAhead);
         else if (PV)
           vt[i + kAhead - kN] = read_vt(vst, i + kAhead - kN);
-        const int kk = i >> 1, mb = i & 1;
+        const int kk = i / kKB, mb = i % kKB;
         s[mb] = (kk == 0) ? mfma32(kf[i], qf[kk], f32x16{}) : mfma32(kf[i], qf[kk], s[mb]);
       }
 #if FASTVR_SCHED
