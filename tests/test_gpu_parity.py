@@ -49,6 +49,11 @@ CASES = [
     ("single_chunk_six_tiles", 1, 1, 128, 1300, 1300, 1300, 0, -1, None, 39),
     ("single_row", 1, 1, 128, 1, 1, 1, 0, -1, None, 40),
     ("kv_longer_than_tile_window", 1, 2, 128, 260, 2600, 260, 9, 3, None, 41),
+    # chunk lengths around the 96-key tile: one key short, exact, one over, two tiles
+    ("chunk95", 1, 2, 128, 600, 600, 95, 0, -1, None, 42),
+    ("chunk96_window2", 1, 2, 128, 768, 768, 96, 0, 2, None, 43),
+    ("chunk97_d64", 1, 2, 64, 700, 700, 97, 0, -1, None, 44),
+    ("chunk192_window1", 1, 2, 128, 960, 960, 192, 0, 1, None, 45),
 ]
 
 
