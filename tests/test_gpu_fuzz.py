@@ -3,6 +3,8 @@ oracle: batch, heads, head_dim, query and key counts, chunk length, chunk
 offset (streaming form), window (the paper's W = 1 among them) and scale are
 drawn per case, so ragged chunks, tiles and tails meet in combinations the
 hand-picked cases do not list."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -15,7 +17,8 @@ from parity import compare, fp32_scale, run_oracle, to_np
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 16
+# more cases for a longer sweep: FASTVR_FUZZ_CASES=200 pytest tests/test_gpu_fuzz.py
+N_CASES = int(os.environ.get("FASTVR_FUZZ_CASES", "24"))
 
 
 def _case(i):
@@ -23,7 +26,7 @@ def _case(i):
     B = int(rng.integers(1, 3))
     H = int(rng.integers(1, 4))
     d = int(rng.choice([64, 128]))
-    L = int(rng.choice([1, 3, 16, 37, 64, 100, 129, 256, 300]))
+    L = int(rng.choice([1, 3, 16, 37, 64, 95, 96, 100, 129, 192, 256, 300]))
     n_chunks = int(rng.integers(1, 6))
     off = int(rng.integers(0, 3))
     nq = int(rng.integers(1, n_chunks * L + 1))
