@@ -76,7 +76,7 @@ constexpr int kStages = 3;                // LDS buffers per operand
 #define FASTVR_PRIO 1
 #endif
 #ifndef FASTVR_AHEAD
-#define FASTVR_AHEAD 6
+#define FASTVR_AHEAD 8
 #endif
 #ifndef FASTVR_VALU_PER
 #define FASTVR_VALU_PER 4
