@@ -45,6 +45,12 @@ namespace {
 
 using namespace dev;
 
+#ifndef FASTVR_BWD_AHEAD
+#define FASTVR_BWD_AHEAD 4  // dK/dV kernel: MFMA operand reads kept in flight ahead (0: the compiler places them)
+#endif
+#ifndef FASTVR_DQ_AHEAD
+#define FASTVR_DQ_AHEAD 4  // dQ kernel: MFMA operand reads kept in flight ahead (0: the compiler places them)
+#endif
 #ifndef FASTVR_PRIO
 #define FASTVR_PRIO 1  // raise the wave priority during matrix-core slots
 #endif
@@ -312,10 +318,35 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
     for (int mb = 0; mb < 2; ++mb) {
       // S^T = K Q^T and dP^T = V dO^T: lane = query n, 16 keys per lane
       f32x16 s, dp;
+      if (FASTVR_DQ_AHEAD > 0) {
+        // MFMA i: k-step i / 2, S^T (even i, K rows) or dP^T (odd i, V rows)
+        constexpr int kN = D / 8;
+        constexpr int kA = FASTVR_DQ_AHEAD < kN ? FASTVR_DQ_AHEAD : kN;
+        u32x4 f[kN];
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        s = mfma32(rd.row(kst, mb, kk), qf[kk], kk == 0 ? f32x16{} : s);
-        dp = mfma32(rd.row(vst, mb, kk), dof[kk], kk == 0 ? f32x16{} : dp);
+        for (int i = 0; i < kA; ++i) f[i] = rd.row((i & 1) ? vst : kst, mb, i >> 1);
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+          if (i + kA < kN) f[i + kA] = rd.row(((i + kA) & 1) ? vst : kst, mb, (i + kA) >> 1);
+          const int kk = i >> 1;
+          if (i & 1)
+            dp = mfma32(f[i], dof[kk], kk == 0 ? f32x16{} : dp);
+          else
+            s = mfma32(f[i], qf[kk], kk == 0 ? f32x16{} : s);
+        }
+        __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kA, 0);
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+          __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+          if (i + kA < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk) {
+          s = mfma32(rd.row(kst, mb, kk), qf[kk], kk == 0 ? f32x16{} : s);
+          dp = mfma32(rd.row(vst, mb, kk), dof[kk], kk == 0 ? f32x16{} : dp);
+        }
       }
       // P^T = exp2(S^T c - LSE log2 e); dS^T = P^T (dP^T - D).  Keys past the
       // interval (last tile only) get P = 0.
@@ -329,10 +360,32 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
       u32x4 dsf[2];
       pack_bf16_half(s, dsf);
       // dQ^T += K^T dS^T over keys 32 mb .. 32 mb + 31
+      if (FASTVR_DQ_AHEAD > 0) {
+        constexpr int kN = 2 * (D / 32);
+        constexpr int kA = FASTVR_DQ_AHEAD < kN ? FASTVR_DQ_AHEAD : kN;
+        u32x4 f[kN];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int gg = 0; gg < 2; ++gg)
+        for (int i = 0; i < kA; ++i) f[i] = rd.tr(kst, 2 * mb + i / (D / 32), i % (D / 32));
 #pragma unroll
-        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(kst, 2 * mb + gg, dm), dsf[gg], acc[dm]);
+        for (int i = 0; i < kN; ++i) {
+          if (i + kA < kN) f[i + kA] = rd.tr(kst, 2 * mb + (i + kA) / (D / 32), (i + kA) % (D / 32));
+          const int gg = i / (D / 32), dm = i % (D / 32);
+          acc[dm] = mfma32(f[i], dsf[gg], acc[dm]);
+        }
+        __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2 * kA, 0);
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+          if (i + kA < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+#pragma unroll
+        for (int gg = 0; gg < 2; ++gg)
+#pragma unroll
+          for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(kst, 2 * mb + gg, dm), dsf[gg], acc[dm]);
+      }
     }
     wait_vmcnt<2 * Dma::kPer>();
     barrier();
@@ -402,25 +455,76 @@ struct Dkv {
   }
   __device__ __forceinline__ const float* rs_stage(int t) const { return rss + (t & (kDkvStages - 1)) * kRs; }
 
+  // sp[mb] (+)= rows 32 mb + n of stage st times kvf (D/16 k-steps x 2 row
+  // blocks), operand reads kA MFMAs ahead
+  template <bool ZERO>
+  __device__ __forceinline__ void row_products(const char* st) {
+    constexpr int kN = D / 8;
+    constexpr int kA = FASTVR_BWD_AHEAD < kN ? FASTVR_BWD_AHEAD : kN;
+    u32x4 f[kN];
+#pragma unroll
+    for (int i = 0; i < kA; ++i) f[i] = rd.row(st, i & 1, i >> 1);
+#pragma unroll
+    for (int i = 0; i < kN; ++i) {
+      if (i + kA < kN) f[i + kA] = rd.row(st, (i + kA) & 1, (i + kA) >> 1);
+      const int kk = i >> 1, mb = i & 1;
+      sp[mb] = mfma32(f[i], kvf[kk], (ZERO && kk == 0) ? f32x16{} : sp[mb]);
+    }
+    __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, kA, 0);
+#pragma unroll
+    for (int i = 0; i < kN; ++i) {
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+      if (i + kA < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // acc[dm] += (stage st)^T k-step g, dims dm * 32 .. times frag[g], operand
+  // reads kA MFMAs ahead
+  __device__ __forceinline__ void tr_products(const char* st) {
+    constexpr int kN = 4 * (D / 32);
+    constexpr int kA = FASTVR_BWD_AHEAD < kN ? FASTVR_BWD_AHEAD : kN;
+    u32x4 f[kN];
+#pragma unroll
+    for (int i = 0; i < kA; ++i) f[i] = rd.tr(st, i / (D / 32), i % (D / 32));
+#pragma unroll
+    for (int i = 0; i < kN; ++i) {
+      if (i + kA < kN) f[i + kA] = rd.tr(st, (i + kA) / (D / 32), (i + kA) % (D / 32));
+      const int g = i / (D / 32), dm = i % (D / 32);
+      acc[dm] = mfma32(f[i], frag[g], acc[dm]);
+    }
+    __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2 * kA, 0);
+#pragma unroll
+    for (int i = 0; i < kN; ++i) {
+      if (i + kA < kN) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(SCHED_MFMA, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
   // Group A, matrix-core slot: S(t) = Q K^T (when S_T) and dV^T += dO^T(t-1) P(t-1) (when PV)
   template <bool S_T, bool PV>
   __device__ __forceinline__ void a_mfma(int t) {
 #if FASTVR_PRIO
     __builtin_amdgcn_s_setprio(1);
 #endif
-    if (S_T) {
-      const char* qst = q_stage(t);
+    if (FASTVR_BWD_AHEAD > 0) {
+      if (S_T) row_products<true>(q_stage(t));
+      if (PV) tr_products(do_stage(t - 1));
+    } else {
+      if (S_T) {
+        const char* qst = q_stage(t);
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
+        for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(qst, mb, kk), kvf[kk], kk == 0 ? f32x16{} : sp[mb]);
-    }
-    if (PV) {
-      const char* dost = do_stage(t - 1);
+          for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(qst, mb, kk), kvf[kk], kk == 0 ? f32x16{} : sp[mb]);
+      }
+      if (PV) {
+        const char* dost = do_stage(t - 1);
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(dost, g, dm), frag[g], acc[dm]);
+          for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(dost, g, dm), frag[g], acc[dm]);
+      }
     }
 #if FASTVR_PRIO
     __builtin_amdgcn_s_setprio(0);
@@ -463,17 +567,26 @@ struct Dkv {
 #pragma unroll
           for (int r = 0; r < 4; ++r) sp[mb][4 * g + r] = d4[r];
         }
+      if (FASTVR_BWD_AHEAD > 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        row_products<false>(dost);
+      } else {
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
+        for (int kk = 0; kk < D / 16; ++kk)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(dost, mb, kk), kvf[kk], sp[mb]);
+          for (int mb = 0; mb < 2; ++mb) sp[mb] = mfma32(rd.row(dost, mb, kk), kvf[kk], sp[mb]);
+      }
     }
     if (DK) {
-      const char* qst = q_stage(t - 1);
+      if (FASTVR_BWD_AHEAD > 0) {
+        tr_products(q_stage(t - 1));
+      } else {
+        const char* qst = q_stage(t - 1);
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(qst, g, dm), frag[g], acc[dm]);
+          for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(qst, g, dm), frag[g], acc[dm]);
+      }
     }
 #if FASTVR_PRIO
     __builtin_amdgcn_s_setprio(0);
