@@ -40,6 +40,8 @@ RING_CASES = [
     ("w3_L4_tiny_chunks", 1, 2, 128, 4 * 9 + 2, 4, 3, 105),
     ("w1_d64_L72", 2, 2, 64, 72 * 5 + 8, 72, 1, 106),
     ("w7_L24", 1, 1, 128, 24 * 10, 24, 7, 107),
+    ("w1_L96_one_tile_per_chunk", 1, 2, 128, 96 * 4 + 50, 96, 1, 108),
+    ("w2_L192_d64", 1, 2, 64, 192 * 4 + 10, 192, 2, 109),
 ]
 
 
