@@ -69,6 +69,8 @@ constexpr int kStages = 3;                // LDS buffers per operand
 //  FASTVR_AHEAD      MFMA operand reads kept in flight ahead of their MFMA
 //  FASTVR_VALU_PER   row-statistics instructions placed after each P.V MFMA
 //  FASTVR_DMA_SPLIT  1: the four vector-ALU waves of a slot issue its DMA; 0: all eight
+//                    (with 96-key tiles only for head_dim 128: a d = 64 tile is 12
+//                    DMA instructions, not a multiple of eight)
 #ifndef FASTVR_SCHED
 #define FASTVR_SCHED 1
 #endif
