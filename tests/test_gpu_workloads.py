@@ -4,7 +4,9 @@ row of every head; 1080p and the wide sliding window a stratified sample of
 query rows, evaluated for every head (every chunk and 256-row tile boundary,
 the ragged tail, and 4096 / 2048 seeded random rows); the 1080p streaming step
 bit for bit against the parallel call over every row and head, and every one of
-its 16320 rows against the oracle for two heads."""
+its 16320 rows against the oracle for two heads; every chunk of the tiny, 1080p
+and wide sliding-window sequences as a streaming call, bit for bit against the
+parallel call."""
 import numpy as np
 import pytest
 import torch
@@ -104,3 +106,29 @@ def test_wide_sliding_window_sampled(dev):
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
     rows = sample_rows(w.n_tokens, w.chunk_len, n_random=2048, seed=5, band=0, tile=1024)
     _check_rows(w, q, k, v, o, lse, rows, "wide_sw")
+
+
+@pytest.mark.parametrize("name", ["tiny", "1080p", "wide_sw"])
+def test_streaming_every_chunk_equals_parallel(dev, name):
+    """Every chunk of the sequence as a streaming call equals the parallel call's
+    rows bit for bit (same key tiles, same arithmetic order).  With a window the
+    cache is compacted to the W + 1 visible chunks and q_chunk_offset is the new
+    chunk's index within it; with W = -1 it holds every earlier chunk."""
+    w = WORKLOADS[name]
+    _announce(f"{name}: every chunk streamed against the parallel call")
+    q, k, v = make_sequence(w)
+    qd, kd, vd, o, lse = _full_call(w, q, k, v, dev)
+    del q, k, v
+    L, N, W = w.chunk_len, w.n_tokens, w.window_chunks
+    n_chunks = (N + L - 1) // L
+    for c in range(n_chunks):
+        c0 = 0 if W < 0 else max(0, c - W)
+        lo, hi = c * L, min((c + 1) * L, N)
+        kc, vc = kd[:, c0 * L:hi].contiguous(), vd[:, c0 * L:hi].contiguous()
+        so, sl = fastvr.chunk_attn(qd[:, lo:hi].contiguous(), kc, vc, chunk_len=L, q_chunk_offset=c - c0,
+                                   window_chunks=W, scale=w.scale)
+        torch.cuda.synchronize()
+        assert torch.equal(so, o[:, lo:hi]), (name, c)
+        assert torch.equal(sl, lse[:, :, lo:hi]), (name, c)
+        del kc, vc, so, sl
+    print(f"[parity] {name}: {n_chunks} streaming calls bit-identical to the parallel call", flush=True)
