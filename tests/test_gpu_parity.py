@@ -200,3 +200,24 @@ def test_bf16_output_is_the_rounded_fp32_output(dev, strided):
     assert torch.equal(l16, l32)
     if strided:
         assert torch.isnan(big[:, :5].float()).all() and torch.isnan(big[:, 5 + N:].float()).all()
+
+
+@pytest.mark.parametrize("W", [-1, 1])
+def test_permuting_keys_within_chunks_leaves_output(dev, W):
+    """Eq. 1 makes attention bidirectional inside a chunk: permuting the keys of
+    every chunk (values permuted the same way) may change only the summation
+    order, so O and LSE move by rounding alone; a stray token-causal mask
+    inside a chunk would change them by O(1)."""
+    B, H, d, N, L = 1, 2, 128, 1000, 250
+    _announce(f"within-chunk key permutation W={W}")
+    q, k, v = make_qkv(B, N, N, H, d, seed=77)
+    g = torch.Generator().manual_seed(78)
+    perm = torch.cat([c * L + torch.randperm(L, generator=g) for c in range(N // L)])
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    o, lse = fastvr.chunk_attn(qd, kd, vd, chunk_len=L, window_chunks=W)
+    op, lp = fastvr.chunk_attn(qd, kd[:, perm.to(dev)].contiguous(), vd[:, perm.to(dev)].contiguous(),
+                               chunk_len=L, window_chunks=W)
+    torch.cuda.synchronize()
+    # bf16 P rounding in a different order: well inside the parity tolerance
+    assert float((o - op).abs().max()) <= 2e-3, float((o - op).abs().max())
+    assert float((lse - lp).abs().max()) <= 1e-4, float((lse - lp).abs().max())
