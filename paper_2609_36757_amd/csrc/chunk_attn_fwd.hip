@@ -18,10 +18,11 @@
 // Matrix-core / vector-ALU ping-pong: waves 0-3 (group A) and 4-7 (group B)
 // share the four SIMDs one-to-one.  Time is cut into slots separated by
 // workgroup barriers, and the two groups swap roles every slot:
-//  * matrix-core slot: the QK MFMAs of key tile j (24 for 96 keys and d = 128),
-//    then the P.V MFMAs of tile j-1 (as many) with the row statistics of the new scores (running maximum, rescale
-//    factor, s * c - m) issued between them, so that this wave's vector-ALU
-//    work hides under its own matrix-core time;
+//  * matrix-core slot: the QK MFMAs of key tile j (24 for 96 keys and
+//    d = 128), then as many P.V MFMAs of tile j-1, with the row statistics of
+//    the new scores (running maximum, rescale factor, s * c - m) issued
+//    between them, so that this wave's vector-ALU work hides under its own
+//    matrix-core time;
 //  * vector-ALU slot: exp2, row sums, bf16 rounding of P and the rescale of O,
 //    plus the DMA of the next K or V tile.
 // Each SIMD therefore always has a matrix-core wave and a vector-ALU wave side
@@ -285,7 +286,8 @@ struct Attn {
     const i32x4 r = {(int)(uint32_t)a, (int)((a >> 32) & 0xffff), rows * st * 2, kBufFlags};
     // per-lane offset within the instruction's rows: drop this wave's row offset
     const uint32_t off = (IS_K ? k_dma_off : v_dma_off) - (uint32_t)((wave % kDmaWaves) * kRowsPerInst * st * 2);
-    const uint32_t la = lds_addr((IS_K ? ks : vs) + stage * kStage) + (uint32_t)((i * kDmaWaves + wave % kDmaWaves) * 64 * 16);
+    const uint32_t la = lds_addr((IS_K ? ks : vs) + stage * kStage) +
+                        (uint32_t)((i * kDmaWaves + wave % kDmaWaves) * 64 * 16);
     dma16(la, off, r, 0);
   }
 
