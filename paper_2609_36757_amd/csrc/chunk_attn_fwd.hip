@@ -44,6 +44,7 @@
 #include <stdint.h>
 
 #include "gfx950_ops.h"
+#include "item_lists.h"
 #include "launch.h"
 
 namespace fastvr {
@@ -121,20 +122,11 @@ __device__ __forceinline__ int vswz(int u) {
   return D >= 128 ? (((u & 1) * 6) ^ ((u >> 1) * 12)) : 2 * u;
 }
 
-// blockIdx -> (local query chunk, batch*head, tile).  Workgroups are handed to
-// the 8 XCDs round-robin; within each full round of 256 workgroups the
-// mapping gives XCD x a run of 32 consecutive items (same batch, head and
-// chunk, i.e. the same K/V stream) so they share that XCD's L2.  Items are
-// ordered by query chunk, last chunk first: under the causal mask later chunks
-// see at least as many keys, so the longest items start first.
-__device__ __forceinline__ void decode_item(const Params& p, int i, int& cl, int& bh, int& t) {
-  constexpr int kRound = 256;
-  int vi = i;
-  const int full = (p.n_items / kRound) * kRound;
-  if (i < full) {
-    const int r = i / kRound, w = i % kRound;
-    vi = r * kRound + (w & 7) * 32 + (w >> 3);
-  }
+// Item index vi -> (local query chunk, batch*head, tile).  Items are ordered by
+// query chunk, last chunk first: under the causal mask later chunks see at
+// least as many keys, so the longest items start first.  (The host's item-list
+// planner decodes item indices the same way.)
+__device__ __forceinline__ void decode_item(const Params& p, int vi, int& cl, int& bh, int& t) {
   const int BH = p.B * p.H;
   const int n_last = BH * p.tiles_last;
   if (vi < n_last) {
@@ -150,6 +142,20 @@ __device__ __forceinline__ void decode_item(const Params& p, int i, int& cl, int
     bh = rem / p.tiles_full;
     t = rem - bh * p.tiles_full;
   }
+}
+
+// blockIdx -> item index.  Workgroups are handed to the 8 XCDs round-robin;
+// within each full round of 256 workgroups the mapping gives XCD x a run of 32
+// consecutive items (same batch, head and chunk, i.e. the same K/V stream) so
+// they share that XCD's L2.
+__device__ __forceinline__ int item_of_block(const Params& p, int i) {
+  constexpr int kRound = 256;
+  const int full = (p.n_items / kRound) * kRound;
+  if (i < full) {
+    const int r = i / kRound, w = i % kRound;
+    return r * kRound + (w & 7) * 32 + (w >> 3);
+  }
+  return i;
 }
 
 template <int D, bool NEG, bool RING>
@@ -518,10 +524,12 @@ struct Attn {
   }
 };
 
+// One work item (a query tile of one batch, head and query chunk) from its
+// decode to its epilogue, run by the whole workgroup; smem is the workgroup's
+// LDS.  Waves without query rows leave before the epilogue.
 template <int D, bool NEG, bool RING>
-__global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Params p) {
+__device__ __forceinline__ void fwd_item(const Params& p, int vi, uint16_t* smem) {
   using A = Attn<D, NEG, RING>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[A::kLdsElems];
   A a;
   a.ks = smem;
   a.vs = smem + kStages * A::kStage;
@@ -534,7 +542,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   const int group = a.wave >> 2;  // 0: waves 0-3, 1: waves 4-7 (one wave of each per SIMD)
 
   int cl, bh, t;
-  decode_item(p, blockIdx.x, cl, bh, t);
+  decode_item(p, vi, cl, bh, t);
   const int b = bh / p.H, h = bh - (bh / p.H) * p.H;
 
   const int L = p.chunk_len;
@@ -744,11 +752,35 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Param
   }
 }
 
+// One workgroup per item, dispatched in item order (longest first).
+template <int D, bool NEG, bool RING>
+__global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_kernel(const Params p) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[Attn<D, NEG, RING>::kLdsElems];
+  fwd_item<D, NEG, RING>(p, item_of_block(p, blockIdx.x), smem);
+}
+
+// One workgroup per CU, each running the items of its own list one after the
+// other (lists planned on the host to even out the CUs' total work).
 template <int D, bool NEG>
-hipError_t launch_t(const Params& p, bool ring, int64_t n_items, hipStream_t stream) {
+__global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_list_kernel(const Params p, const ItemLists lst) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[Attn<D, NEG, false>::kLdsElems];
+  const int g = blockIdx.x;
+  for (int u = lst.start[g]; u < lst.start[g + 1]; ++u) {
+    fwd_item<D, NEG, false>(p, lst.item[u], smem);
+    // every wave is done with the item's LDS stages before the next item's DMA
+    barrier();
+  }
+}
+
+template <int D, bool NEG>
+hipError_t launch_t(const Params& p, bool ring, int64_t n_items, const ItemLists* lists, int n_groups,
+                    hipStream_t stream) {
   if (ring)
     hipLaunchKernelGGL((chunk_attn_fwd_kernel<D, NEG, true>), dim3((unsigned)n_items), dim3(kFwdThreads), 0, stream,
                        p);
+  else if (lists != nullptr)
+    hipLaunchKernelGGL((chunk_attn_fwd_list_kernel<D, NEG>), dim3((unsigned)n_groups), dim3(kFwdThreads), 0, stream,
+                       p, *lists);
   else
     hipLaunchKernelGGL((chunk_attn_fwd_kernel<D, NEG, false>), dim3((unsigned)n_items), dim3(kFwdThreads), 0, stream,
                        p);
@@ -808,9 +840,23 @@ hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   p.new_slot = (int32_t)a.new_slot;
   p.ring_chunk = (int32_t)a.chunk_len;
   const bool neg = p.c < 0.f;
+  // a few uneven items per CU: per-CU item lists (the CU count of the current
+  // device; any failure to query it keeps plain dispatch)
+  ItemLists lists;
+  const ItemLists* use_lists = nullptr;
+  int n_groups = 0;
+  int dev = 0, n_cu = 0;
+  if (!ring && g.n_items <= kListMaxItems && hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) {
+    const ItemShape shape{(int64_t)p.B * p.H, p.n_local_chunks, p.tiles_full, p.tiles_last, p.chunk_len,
+                          p.q_chunk_offset, p.window, p.nkv, kBK};
+    if (plan_item_lists(shape, (int)g.n_items, n_cu, &lists, &n_groups)) use_lists = &lists;
+  }
   if (a.d == 128)
-    return neg ? launch_t<128, true>(p, ring, g.n_items, stream) : launch_t<128, false>(p, ring, g.n_items, stream);
-  return neg ? launch_t<64, true>(p, ring, g.n_items, stream) : launch_t<64, false>(p, ring, g.n_items, stream);
+    return neg ? launch_t<128, true>(p, ring, g.n_items, use_lists, n_groups, stream)
+               : launch_t<128, false>(p, ring, g.n_items, use_lists, n_groups, stream);
+  return neg ? launch_t<64, true>(p, ring, g.n_items, use_lists, n_groups, stream)
+             : launch_t<64, false>(p, ring, g.n_items, use_lists, n_groups, stream);
 }
 
 }  // namespace fastvr

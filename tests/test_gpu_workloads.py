@@ -108,10 +108,12 @@ def test_wide_sliding_window_sampled(dev):
     _check_rows(w, q, k, v, o, lse, rows, "wide_sw")
 
 
-@pytest.mark.parametrize("name", ["tiny", "1080p", "wide_sw"])
+@pytest.mark.parametrize("name", ["tiny", "480p", "1080p", "wide_sw"])
 def test_streaming_every_chunk_equals_parallel(dev, name):
     """Every chunk of the sequence as a streaming call equals the parallel call's
-    rows bit for bit (same key tiles, same arithmetic order).  With a window the
+    rows bit for bit (same key tiles, same arithmetic order).  For 480p the
+    parallel call (936 items) runs as per-CU item lists and each streaming call
+    (156 items) as plain dispatch, so this also checks the list kernel.  With a window the
     cache is compacted to the W + 1 visible chunks and q_chunk_offset is the new
     chunk's index within it; with W = -1 it holds every earlier chunk."""
     w = WORKLOADS[name]
