@@ -228,14 +228,14 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     streaming step with the bounded ring cache at the 1080p chunk shape."""
     from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence
     res = {}
-    for name, reps in (("tiny", 50), ("480p", 20), ("wide_sw", 3)):
+    for name, reps in (("tiny", 200), ("480p", 100), ("wide_sw", 3)):
         w = WORKLOADS[name]
         q, k, v = (t.to(dev) for t in make_sequence(w))
         o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
         lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
         ms = _time_ms(torch, cur, lambda: fastvr.chunk_attn(q, k, v, chunk_len=w.chunk_len,
                                                             window_chunks=w.window_chunks, scale=w.scale,
-                                                            out=o, lse=lse), reps)
+                                                            out=o, lse=lse), reps, warm=5)
         f = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
         res[name] = {"ms": round(ms, 4), "ms_per_chunk": round(ms / w.n_chunks, 4),
                      "tflops": round(f / (ms * 1e-3) / 1e12, 2), "frac_of_bf16_peak": round(f / (ms * 1e-3) / 1e12
