@@ -9,7 +9,9 @@
 //
 // Work decomposition: one workgroup (8 wave64, 512 threads) per
 // (batch, head, query chunk, 256-row query tile); tiles never straddle a chunk.
-// Each wave owns 32 query rows.  Scores are computed transposed,
+// Items are dispatched longest first; when they are few per CU and uneven, the
+// host instead packs them into one list per CU and launches one workgroup per
+// CU that runs its list (item_lists.h).  Each wave owns 32 query rows.  Scores are computed transposed,
 // S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the accumulator puts one query per
 // lane (column) and 16 keys per lane (rows), so row max and row sum are in-lane
 // plus one exchange between the two 32-lane halves.  The same registers,
