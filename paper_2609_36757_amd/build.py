@@ -17,7 +17,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libfastvr.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
-SOURCES = ["chunk_attn_fwd.hip", "chunk_attn_bwd.hip", "kv_append.hip", "one_step.hip", "tiles.hip", "fastvr_api.cpp"]
+SOURCES = ["chunk_attn_fwd.hip", "chunk_attn_bwd.hip", "kv_append.hip", "one_step.hip", "tiles.hip", "fastvr_api.cpp",
+           "geometry.cpp"]
 ARCH = "gfx950"
 
 

@@ -789,19 +789,6 @@ hipError_t launch_bwd_t(const BwdParams& p, hipStream_t stream) {
 
 }  // namespace
 
-BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len) {
-  BwdGrid g{};
-  const int64_t L = chunk_len > nkv ? nkv : chunk_len;
-  g.q = fwd_grid(B, H, nq, L);
-  if (B <= 0 || H <= 0 || nkv <= 0 || L <= 0) return g;
-  g.n_kchunks = (nkv + L - 1) / L;
-  const int64_t last_keys = nkv - (g.n_kchunks - 1) * L;
-  g.kblocks_last = (last_keys + kBwdKeysPerItem - 1) / kBwdKeysPerItem;
-  g.kblocks_full = g.n_kchunks > 1 ? (L + kBwdKeysPerItem - 1) / kBwdKeysPerItem : g.kblocks_last;
-  g.n_kv_items = B * H * (g.kblocks_last + g.kblocks_full * (g.n_kchunks - 1));
-  return g;
-}
-
 hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream) {
   const BwdGrid g = bwd_grid(a.B, a.H, a.nq, a.nkv, a.chunk_len);
   BwdParams p;

@@ -45,6 +45,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "gfx950_ops.h"
 #include "item_lists.h"
 #include "launch.h"
@@ -789,18 +791,25 @@ hipError_t launch_t(const Params& p, bool ring, int64_t n_items, const ItemLists
   return hipGetLastError();
 }
 
-}  // namespace
-
-FwdGrid fwd_grid(int64_t B, int64_t H, int64_t nq, int64_t chunk_len) {
-  FwdGrid g{};
-  if (B <= 0 || H <= 0 || nq <= 0 || chunk_len <= 0) return g;
-  g.n_local_chunks = (nq + chunk_len - 1) / chunk_len;
-  const int64_t last_rows = nq - (g.n_local_chunks - 1) * chunk_len;
-  g.tiles_last = (last_rows + kBQ - 1) / kBQ;
-  g.tiles_full = g.n_local_chunks > 1 ? (chunk_len + kBQ - 1) / kBQ : g.tiles_last;
-  g.n_items = B * H * (g.tiles_last + g.tiles_full * (g.n_local_chunks - 1));
-  return g;
+// CU count of the current device, queried once per device (0 if it cannot be read)
+int device_cu_count() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cus[kMaxDevices];  // 0: not queried yet, -1: query failed
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev >= kMaxDevices) {
+    int n = 0;
+    return hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess ? n : 0;
+  }
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = -1;
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n > 0 ? n : 0;
 }
+
+}  // namespace
 
 hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   const FwdGrid g = fwd_grid(a.B, a.H, a.nq, a.chunk_len > a.nkv ? a.nkv : a.chunk_len);
@@ -847,12 +856,12 @@ hipError_t launch_chunk_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   ItemLists lists;
   const ItemLists* use_lists = nullptr;
   int n_groups = 0;
-  int dev = 0, n_cu = 0;
-  if (!ring && g.n_items <= kListMaxItems && hipGetDevice(&dev) == hipSuccess &&
-      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) {
+  int n_cu = 0;
+  if (!ring && g.n_items > 0 && g.n_items <= kListMaxItems && (n_cu = device_cu_count()) > 0) {
     const ItemShape shape{(int64_t)p.B * p.H, p.n_local_chunks, p.tiles_full, p.tiles_last, p.chunk_len,
                           p.q_chunk_offset, p.window, p.nkv, kBK};
-    if (plan_item_lists(shape, (int)g.n_items, n_cu, &lists, &n_groups)) use_lists = &lists;
+    static PlanCache plans;
+    if (plans.plan(shape, (int)g.n_items, n_cu, &lists, &n_groups)) use_lists = &lists;
   }
   if (a.d == 128)
     return neg ? launch_t<128, true>(p, ring, g.n_items, use_lists, n_groups, stream)

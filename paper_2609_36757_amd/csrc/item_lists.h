@@ -14,6 +14,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 namespace fastvr {
 
@@ -158,5 +159,60 @@ inline bool plan_item_lists(const ItemShape& s, int n_items, int n_cu, ItemLists
   *n_groups = n_cu;
   return true;
 }
+
+inline bool same_shape(const ItemShape& a, const ItemShape& b) {
+  return a.bh == b.bh && a.n_local_chunks == b.n_local_chunks && a.tiles_full == b.tiles_full &&
+         a.tiles_last == b.tiles_last && a.chunk_len == b.chunk_len && a.q_chunk_offset == b.q_chunk_offset &&
+         a.window == b.window && a.nkv == b.nkv && a.key_tile == b.key_tile;
+}
+
+// The last few plans (positive and negative decisions alike), so that a caller
+// repeating one call shape plans it once.  Thread-safe; entries are replaced
+// round-robin.  A plan depends only on the shape, the item count and the CU
+// count, all part of the key.
+class PlanCache {
+ public:
+  static constexpr int kEntries = 8;
+  bool plan(const ItemShape& s, int n_items, int n_cu, ItemLists* out, int* n_groups) {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      for (int e = 0; e < kEntries; ++e) {
+        const Entry& x = ent_[e];
+        if (x.valid && x.n_items == n_items && x.n_cu == n_cu && same_shape(x.shape, s)) {
+          if (x.used) {
+            *out = x.lists;
+            *n_groups = x.n_groups;
+          }
+          return x.used;
+        }
+      }
+    }
+    Entry fresh;
+    fresh.shape = s;
+    fresh.n_items = n_items;
+    fresh.n_cu = n_cu;
+    fresh.used = plan_item_lists(s, n_items, n_cu, &fresh.lists, &fresh.n_groups);
+    fresh.valid = true;
+    if (fresh.used) {
+      *out = fresh.lists;
+      *n_groups = fresh.n_groups;
+    }
+    std::lock_guard<std::mutex> g(mu_);
+    ent_[next_] = fresh;
+    next_ = (next_ + 1) % kEntries;
+    return fresh.used;
+  }
+
+ private:
+  struct Entry {
+    ItemShape shape{};
+    int n_items = 0, n_cu = 0, n_groups = 0;
+    bool valid = false, used = false;
+    ItemLists lists;
+  };
+  std::mutex mu_;
+  Entry ent_[kEntries];
+  int next_ = 0;
+};
 
 }  // namespace fastvr

@@ -195,14 +195,6 @@ unsigned grid_for(int64_t rows) { return (unsigned)(rows < 8192 ? (rows < 1 ? 1 
 
 }  // namespace
 
-TileAxis tile_axis(int64_t size, int64_t tile, int64_t overlap) {
-  TileAxis a{};
-  if (size < 1 || tile < 1 || overlap < 0 || overlap >= tile) return a;
-  a.len = size < tile ? size : tile;
-  a.n = size <= tile ? 1 : (size - overlap + (tile - overlap) - 1) / (tile - overlap);
-  return a;
-}
-
 hipError_t launch_tile_gather(const void* x, void* tiles, int64_t B, int64_t T, int64_t Hg, int64_t Wg, int64_t C,
                               int64_t tile, int64_t overlap, hipStream_t stream) {
   const Axis ay = make_axis(Hg, tile, overlap), ax = make_axis(Wg, tile, overlap);

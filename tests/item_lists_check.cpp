@@ -6,6 +6,7 @@
 // g % 8).  Prints one line per case; exits non-zero on the first failure.
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include <random>
 #include <vector>
@@ -76,6 +77,9 @@ int main() {
   // a CU count that is not a multiple of 8, and a small one
   if (check(c++, ItemShape{12, 6, 13, 13, 3120, 0, -1, 18720, 96}, 100, -1)) return 1;
   if (check(c++, ItemShape{12, 6, 13, 13, 3120, 0, -1, 18720, 96}, 8, 0)) return 1;
+  // the GPU zero-fill test's list-kernel shape: 4 chunks of 3120 tokens and a
+  // last chunk of 770 (4 tiles), 672 items; it must take the list kernel
+  if (check(c++, ItemShape{12, 5, 13, 4, 3120, 0, -1, 13250, 96}, 256, 1)) return 1;
   // seeded random shapes: windows, offsets, ragged last chunks
   std::mt19937 rng(1234);
   for (int r = 0; r < 400; ++r) {
@@ -87,6 +91,25 @@ int main() {
     const ItemShape s{bh, nch, nch > 1 ? tf : tl, tl, L, off, W, nkv, 96};
     const int n_cu = (rng() % 4 == 0) ? 8 * (1 + rng() % 32) : 256;
     if (check(c++, s, n_cu, -1)) return 1;
+  }
+  // the plan cache returns what a fresh plan gives, hits and misses alike
+  // (12 shapes cycled three times through its 8 entries, both decisions)
+  {
+    static fastvr::PlanCache cache;
+    static ItemLists a, b;
+    for (int rep = 0; rep < 36; ++rep) {
+      const int r = rep % 12;
+      const ItemShape s{12, 6 - r % 3, 13, 13 - r / 3, 3120, 0, r % 2 ? -1 : 2, 18720, 96};
+      const int n = (int)n_items_of(s);
+      int ga = 0, gb = 0;
+      const bool ua = fastvr::plan_item_lists(s, n, 256, &a, &ga);
+      const bool ub = cache.plan(s, n, 256, &b, &gb);
+      if (ua != ub) return fail("plan cache decision differs", c);
+      if (ua && (ga != gb || memcmp(a.start, b.start, sizeof(a.start)) != 0 ||
+                 memcmp(a.item, b.item, sizeof(uint16_t) * n) != 0))
+        return fail("plan cache lists differ", c);
+    }
+    ++c;
   }
   printf("all %d cases ok\n", c);
   return 0;

@@ -71,3 +71,62 @@ def to_np(t: torch.Tensor) -> np.ndarray:
 
 def default_scale(d: int) -> float:
     return 1.0 / math.sqrt(d)
+
+
+def oracle_workers() -> int:
+    """Host threads for the oracle: the CPU share of one GPU (16) at most."""
+    import os
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def run_oracle_parallel(q, k, v, chunk_len, q_chunk_offset, window_chunks, scale, rows=None, heads=None,
+                        block=1024, workers=None):
+    """The fp64 oracle on many rows at once, in host threads (NumPy releases the
+    GIL inside BLAS and its element-wise loops; BLAS itself runs one thread per
+    worker).  Work units are (head, query chunk, block of rows).  Each unit hands
+    the oracle only the keys its chunk can see, [max(0, c - W) L, min((c + 1) L,
+    Nkv)), with q_chunk_offset measured from the first of them: the mask depends
+    only on chunk differences, so this is the same function (the oracle's
+    compacted-cache pin checks exactly that), at the cost of the visible keys.
+
+    Returns (o [B, R, Hs, d], lse [B, Hs, R]) for the rows (sorted, all rows if
+    None) and heads (all if None) asked for."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from threadpoolctl import threadpool_limits
+
+    B, nq, H, d = q.shape
+    nkv = k.shape[1]
+    L = int(chunk_len)
+    W = int(window_chunks)
+    rows = np.arange(nq, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    assert np.all(np.diff(rows) > 0), "rows must be sorted and distinct"
+    heads = list(range(H)) if heads is None else list(heads)
+    s32 = fp32_scale(scale)
+    units = []
+    cl = rows // L
+    for local in np.unique(cl):
+        idx = np.nonzero(cl == local)[0]
+        c = q_chunk_offset + int(local)
+        lo = max(0, c - W) * L if W >= 0 else 0
+        hi = min((c + 1) * L, nkv)
+        for hi_pos, h in enumerate(heads):
+            for b0 in range(0, len(idx), block):
+                units.append((hi_pos, h, idx[b0:b0 + block], int(local), c, lo, hi))
+    o = np.zeros((B, len(rows), len(heads), d))
+    lse = np.zeros((B, len(heads), len(rows)))
+
+    def job(u):
+        hp, h, idx, local, c, lo, hi = u
+        qs = q[:, local * L:min((local + 1) * L, nq), h:h + 1]
+        ks, vs = k[:, lo:hi, h:h + 1], v[:, lo:hi, h:h + 1]
+        oo, ll = oracle.attention(qs, ks, vs, chunk_len=L, q_chunk_offset=c - lo // L, window_chunks=W,
+                                  scale=s32, rows=rows[idx] - local * L)
+        o[:, idx, hp] = oo[:, :, 0]
+        lse[:, hp, idx] = ll[:, 0]
+
+    with threadpool_limits(1, "blas"):
+        with ThreadPoolExecutor(workers or oracle_workers()) as ex:
+            for _ in ex.map(job, units):
+                pass
+    return o, lse

@@ -8,7 +8,6 @@ import re
 import pytest
 
 from paper_2609_36757_amd import fastvr
-from paper_2609_36757_amd import workloads
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fastvr.h")
 
@@ -347,6 +346,41 @@ def test_tile_empty_is_ok(lib, kw):
     assert _tb(update=True, **kw) == fastvr.OK
 
 
+def test_valid_calls_reach_the_launcher(lib):
+    """Valid arguments pass every check and reach the launcher.  Runs only
+    against the host-only build whose launchers are stand-ins that launch
+    nothing (tests/host_stubs.cpp, built by tests/test_host_sanitizers.py), so
+    the fake addresses are never used; the real library is skipped."""
+    if not hasattr(lib, "fastvr_stub_launch_count"):
+        pytest.skip("needs the host-only build with stand-in launchers")
+    lib.fastvr_stub_launch_count.restype = ctypes.c_int64
+    calls = [
+        lambda: _fwd(),
+        lambda: _fwd(d=128, window_chunks=1, Nkv=200, chunk_len=64),
+        lambda: _fwd(lse=None, q_chunk_offset=2, Nq=16, Nkv=64),
+        lambda: _fwd_ex(),
+        lambda: _fwd_ex(o_bf16=1, o_st=136, o_sb=64 * 136, k_sb=100 * 128, v_sb=100 * 128, Nkv=100),
+        lambda: _app(),
+        lambda: _app(B=3, d=128, cache_len=0, n_new=100),
+        lambda: _ring(),
+        lambda: _ring(chunk_index=0, window_chunks=0, n_new=5, chunk_len=64),
+        lambda: _ring(d=64, chunk_len=72, n_new=72, chunk_index=9, window_chunks=7),
+        lambda: _bwd(),
+        lambda: _bwd(d=128, Nq=16, Nkv=64, q_chunk_offset=3, window_chunks=1),
+        lambda: _bwd(Nq=0, q=None, dout=None, o=None, dq=None, lse=None, rs=None),
+        lambda: _os(),
+        lambda: _os(out=Z, out_bf16=1),
+        lambda: _tg(),
+        lambda: _tb(),
+        lambda: _tb(update=True),
+    ]
+    for i, call in enumerate(calls):
+        before = lib.fastvr_stub_launch_count()
+        assert call() == fastvr.OK, (i, fastvr.last_error())
+        assert fastvr.last_error() == ""
+        assert lib.fastvr_stub_launch_count() == before + 1, i
+
+
 def test_error_is_thread_local(lib):
     import threading
     assert _fwd(d=96) == fastvr.ERR_UNSUPPORTED
@@ -369,6 +403,7 @@ def test_wrapper_fails_loudly_without_library(monkeypatch):
 
 
 def test_input_generator_is_deterministic():
+    from paper_2609_36757_amd import workloads
     a = workloads.make_qkv(1, 33, 40, 2, 64, seed=9)
     b = workloads.make_qkv(1, 33, 40, 2, 64, seed=9)
     c = workloads.make_qkv(1, 33, 40, 2, 64, seed=10)
@@ -379,6 +414,7 @@ def test_input_generator_is_deterministic():
 
 
 def test_workload_registry_shapes():
+    from paper_2609_36757_amd import workloads
     w = workloads.WORKLOADS
     assert (w["1080p"].n_tokens, w["1080p"].chunk_len, w["1080p"].n_chunks) == (65280, 16320, 4)
     assert (w["480p"].n_tokens, w["480p"].chunk_len, w["480p"].n_chunks) == (18720, 3120, 6)

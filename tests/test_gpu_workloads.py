@@ -1,12 +1,18 @@
 """Parity at the full sizes of the benchmark workloads, in the launch
-configuration the benchmark times.  Coverage per workload: tiny and 480p every
-row of every head; 1080p and the wide sliding window a stratified sample of
-query rows, evaluated for every head (every chunk and 256-row tile boundary,
-the ragged tail, and 4096 / 2048 seeded random rows); the 1080p streaming step
-bit for bit against the parallel call over every row and head, and every one of
-its 16320 rows against the oracle for two heads; every chunk of the tiny, 1080p
-and wide sliding-window sequences as a streaming call, bit for bit against the
-parallel call."""
+configuration the benchmark times.  Coverage per workload, every head each time:
+
+* tiny and 480p: every row against the fp64 oracle;
+* 1080p streaming step: every one of its 16320 rows against the oracle, and
+  bit for bit against the rows of the parallel call;
+* 1080p parallel call and the wide sliding window: a stratified row sample
+  against the oracle, holding every row within 2 of each chunk boundary and of
+  each 256-row query-tile boundary (the kernel's tile), the last rows of every
+  chunk (the ragged tail included) and 4096 seeded random rows;
+* every chunk of the tiny, 1080p and wide sliding-window sequences as a
+  streaming call, bit for bit against the parallel call.
+
+The oracle runs in host threads, each query chunk against the keys it can see
+(parity.run_oracle_parallel)."""
 import numpy as np
 import pytest
 import torch
@@ -14,7 +20,7 @@ import torch
 from paper_2609_36757_amd import fastvr
 from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence, streaming_views
 
-from parity import compare, run_oracle, sample_rows, to_np
+from parity import compare, run_oracle_parallel, sample_rows, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -43,7 +49,7 @@ def _check_rows(w, q, k, v, o, lse, rows, label, q_chunk_offset=0):
     o_s = to_np(o[:, ridx])
     l_s = to_np(lse[:, :, ridx])
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
-    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, q_chunk_offset, w.window_chunks, w.scale, rows=rows)
+    o_ref, l_ref = run_oracle_parallel(q, k, v, w.chunk_len, q_chunk_offset, w.window_chunks, w.scale, rows=rows)
     return compare(o_s, l_s, o_ref, l_ref, label=f"{label} ({len(rows)} rows)")
 
 
@@ -52,7 +58,7 @@ def test_tiny_all_rows(dev):
     _announce("tiny B=1 H=2 d=64 N=1024 L=256")
     q, k, v = make_sequence(w)
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
-    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
+    o_ref, l_ref = run_oracle_parallel(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
     compare(to_np(o), to_np(lse), o_ref, l_ref, label="tiny (all rows)")
 
 
@@ -61,8 +67,8 @@ def test_480p_all_rows(dev):
     _announce("480p B=1 H=12 d=128 N=18720 L=3120 (all rows)")
     q, k, v = make_sequence(w)
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
-    o_ref, l_ref = run_oracle(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
-    compare(to_np(o), to_np(lse), o_ref, l_ref, label="480p (all rows)")
+    o_ref, l_ref = run_oracle_parallel(q, k, v, w.chunk_len, 0, w.window_chunks, w.scale)
+    compare(to_np(o), to_np(lse), o_ref, l_ref, label="480p (all rows, all heads)")
 
 
 def test_1080p_full_and_streaming_step(dev):
@@ -71,7 +77,7 @@ def test_1080p_full_and_streaming_step(dev):
     _announce("1080p B=1 H=12 d=128 N=65280 L=16320 + streaming step chunk 3")
     q, k, v = make_sequence(w)
     qd, kd, vd, o, lse = _full_call(w, q, k, v, dev)
-    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=4096, seed=3, band=0)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=4096, seed=3, band=2, tile=256)
     _check_rows(w, q, k, v, o, lse, rows, "1080p")
 
     # streaming step: cache holds chunks 0-2, append chunk 3, attend chunk 3
@@ -90,13 +96,11 @@ def test_1080p_full_and_streaming_step(dev):
     assert torch.equal(kc, kd) and torch.equal(vc, vd)
     assert torch.equal(so, o[:, lo:lo + so.shape[1]]), "streaming step differs from the parallel call"
     assert torch.equal(sl, lse[:, :, lo:lo + so.shape[1]])
-    # every row of the streaming step, two heads
-    heads = [0, 7]
-    hs = torch.as_tensor(heads, device=so.device)
-    o_ref, l_ref = run_oracle(q[:, lo:lo + so.shape[1], heads], k[:, :, heads], v[:, :, heads], ws.chunk_len,
-                              sv["q_chunk_offset"], ws.window_chunks, ws.scale)
-    compare(to_np(so[:, :, hs]), to_np(sl[:, hs]), o_ref, l_ref,
-            label=f"1080p streaming step (all {so.shape[1]} rows, heads {heads})")
+    # every row of the streaming step, every head
+    o_ref, l_ref = run_oracle_parallel(q[:, lo:lo + so.shape[1]], k, v, ws.chunk_len, sv["q_chunk_offset"],
+                                       ws.window_chunks, ws.scale)
+    compare(to_np(so), to_np(sl), o_ref, l_ref,
+            label=f"1080p streaming step (all {so.shape[1]} rows, all {w.H} heads)")
 
 
 def test_wide_sliding_window_sampled(dev):
@@ -104,7 +108,7 @@ def test_wide_sliding_window_sampled(dev):
     _announce("wide_sw B=1 H=24 d=128 N=138720 L=16320 W=2 outliers")
     q, k, v = make_sequence(w)
     _, _, _, o, lse = _full_call(w, q, k, v, dev)
-    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=2048, seed=5, band=0, tile=1024)
+    rows = sample_rows(w.n_tokens, w.chunk_len, n_random=4096, seed=5, band=2, tile=256)
     _check_rows(w, q, k, v, o, lse, rows, "wide_sw")
 
 
