@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define FASTVR_ABI_VERSION 6
+#define FASTVR_ABI_VERSION 7
 
 typedef enum {
   FASTVR_OK = 0,
@@ -186,6 +186,31 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
                                     const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
                                     int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
                                     int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream);
+
+/*
+ * fastvr_chunk_attn_bwd without the row_stats workspace argument, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving or training loops, harnesses that forbid allocation).  The row
+ * statistics go to a static array of the library instead, 32 MiB
+ * (FASTVR_BWD_NOALLOC_MAX_FLOATS floats) that each device holds from the first
+ * call until the process ends; the call itself allocates nothing (no hipMalloc,
+ * no allocating library routine).  The caller still passes every input and
+ * output, with the same meaning, layout and preconditions as in
+ * fastvr_chunk_attn_bwd; outputs are identical bit for bit.
+ *
+ * Limit: 2 * B * H * Nq <= FASTVR_BWD_NOALLOC_MAX_FLOATS, else
+ * FASTVR_ERR_UNSUPPORTED (the 1080p sequence needs 1.6 M floats, the 24-head
+ * sliding-window sequence 6.7 M).  Every call on one device shares the array:
+ * calls that may overlap in time on the same device (different streams or host
+ * threads) race and must be serialised by the caller.  FASTVR_ERR_HIP if the
+ * array's device address cannot be obtained.
+ */
+#define FASTVR_BWD_NOALLOC_MAX_FLOATS (8 * 1024 * 1024)
+fastvr_status fastvr_chunk_attn_bwd_noalloc(const void* q, const void* k, const void* v, const float* o,
+                                            const float* lse, const void* dout, float* dq, float* dk, float* dv,
+                                            int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                                            int64_t chunk_len, int64_t q_chunk_offset, int64_t window_chunks,
+                                            float scale, void* stream);
 
 /*
  * One-step latent update (Sec. 3.2, Eq. 9, the update used at inference, Sec.

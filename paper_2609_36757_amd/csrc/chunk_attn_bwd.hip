@@ -37,6 +37,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "gfx950_ops.h"
 #include "launch.h"
 
@@ -827,6 +829,35 @@ hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream) {
   p.scale = a.scale;
   if (a.d == 128) return launch_bwd_t<128>(p, stream);
   return launch_bwd_t<64>(p, stream);
+}
+
+// Workspace of the allocation-free backward (fastvr_chunk_attn_bwd_noalloc):
+// the row statistics [B, H, 2, Nq] live in this array instead of caller
+// memory.  Each device holds its own copy from the first load of the library's
+// code object until the process ends; every call on a device shares it.  The
+// dQ kernel writes every entry the dK/dV kernel reads before it reads them
+// (same stream), so nothing has to start at zero.
+static __device__ __align__(256) float scratch[kBwdScratchFloats];
+
+// Device address of this device's copy of `scratch` (host code must not use
+// the array's name as an address): looked up once per device, with that
+// device current, and kept.
+hipError_t bwd_scratch(float** out) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<float*> addr[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  float* p = addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    e = hipGetSymbolAddress(reinterpret_cast<void**>(&p), HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return hipSuccess;
 }
 
 }  // namespace fastvr

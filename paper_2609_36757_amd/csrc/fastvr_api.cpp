@@ -260,10 +260,17 @@ fastvr_status fastvr_chunk_attn_ring_step(const void* q_new, const void* k_new, 
                   n_prev, window_chunks, scale, stream, r);
 }
 
-fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
-                                    const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
-                                    int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
-                                    int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The backward's checks and launch.  own_ws: row_stats is ignored and the
+// row statistics go to the library's static per-device array (looked up after
+// every check has passed).
+fastvr_status bwd_impl(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                       const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B, int64_t H,
+                       int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len, int64_t q_chunk_offset,
+                       int64_t window_chunks, float scale, void* stream, bool own_ws) {
   if (B < 0 || H < 0 || Nq < 0 || Nkv < 0)
     return fail(FASTVR_ERR_INVALID_ARGUMENT, "negative size (B=%lld H=%lld Nq=%lld Nkv=%lld)", (long long)B,
                 (long long)H, (long long)Nq, (long long)Nkv);
@@ -313,14 +320,25 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
     if ((s = check_view(views[i], B, hd, &bytes[i])) != FASTVR_OK) return s;
   }
   const void* lse_ptr = lse;
-  const void* rs_ptr = row_stats;
+  const void* rs_ptr = own_ws ? nullptr : row_stats;
   if (Nq > 0) {
-    if (lse == nullptr || row_stats == nullptr)
-      return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is NULL");
-    if (!aligned(lse, 4) || !aligned(row_stats, 4))
-      return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is not 4-byte aligned");
-    if (!mul_ok(nrows, 4, &bytes[8]) || !mul_ok(nrows, 8, &bytes[9]))
-      return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+    if (own_ws) {
+      if (lse == nullptr) return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse is NULL");
+      if (!aligned(lse, 4)) return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse is not 4-byte aligned");
+      if (!mul_ok(nrows, 4, &bytes[8])) return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+      if (nrows > fastvr::kBwdScratchFloats / 2)
+        return fail(FASTVR_ERR_UNSUPPORTED,
+                    "row statistics need 2 * B * H * Nq = %lld floats; the allocation-free backward holds at most "
+                    "%lld",
+                    (long long)(2 * nrows), (long long)fastvr::kBwdScratchFloats);
+    } else {
+      if (lse == nullptr || row_stats == nullptr)
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is NULL");
+      if (!aligned(lse, 4) || !aligned(row_stats, 4))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "lse or row_stats is not 4-byte aligned");
+      if (!mul_ok(nrows, 4, &bytes[8]) || !mul_ok(nrows, 8, &bytes[9]))
+        return fail(FASTVR_ERR_INVALID_ARGUMENT, "size overflows int64");
+    }
   }
   // outputs (dq, dk, dv, row_stats) overlap nothing else
   const void* ptrs[10] = {q, dout, o, dq, k, v, dk, dv, lse_ptr, rs_ptr};
@@ -338,6 +356,11 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
   if (g.q.n_items > fastvr::kMaxFwdItems || g.n_kv_items > fastvr::kMaxFwdItems)
     return fail(FASTVR_ERR_UNSUPPORTED, "problem needs too many workgroups");
 
+  if (own_ws && Nq > 0) {
+    const hipError_t e = fastvr::bwd_scratch(&row_stats);
+    if (e != hipSuccess)
+      return fail(FASTVR_ERR_HIP, "workspace of the allocation-free backward: %s", hipGetErrorString(e));
+  }
   fastvr::BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.dout = dout; a.o = o; a.lse = lse;
   a.dq = dq; a.dk = dk; a.dv = dv; a.row_stats = row_stats;
@@ -349,6 +372,27 @@ fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v,
   const hipError_t e = fastvr::launch_chunk_attn_bwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(FASTVR_ERR_HIP, "chunk_attn_bwd launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+fastvr_status fastvr_chunk_attn_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                                    const void* dout, float* dq, float* dk, float* dv, float* row_stats, int64_t B,
+                                    int64_t H, int64_t Nq, int64_t Nkv, int64_t d, int64_t chunk_len,
+                                    int64_t q_chunk_offset, int64_t window_chunks, float scale, void* stream) {
+  return bwd_impl(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+                  window_chunks, scale, stream, false);
+}
+
+fastvr_status fastvr_chunk_attn_bwd_noalloc(const void* q, const void* k, const void* v, const float* o,
+                                            const float* lse, const void* dout, float* dq, float* dk, float* dv,
+                                            int64_t B, int64_t H, int64_t Nq, int64_t Nkv, int64_t d,
+                                            int64_t chunk_len, int64_t q_chunk_offset, int64_t window_chunks,
+                                            float scale, void* stream) {
+  return bwd_impl(q, k, v, o, lse, dout, dq, dk, dv, nullptr, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+                  window_chunks, scale, stream, true);
 }
 
 fastvr_status fastvr_kv_cache_append(void* k_cache, void* v_cache, const void* k_new, const void* v_new, int64_t B,

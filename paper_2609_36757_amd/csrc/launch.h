@@ -5,6 +5,8 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "fastvr.h"
+
 namespace fastvr {
 
 struct FwdArgs {
@@ -82,6 +84,12 @@ constexpr int kBwdKeysPerItem = 128;
 
 BwdGrid bwd_grid(int64_t B, int64_t H, int64_t nq, int64_t nkv, int64_t chunk_len);
 hipError_t launch_chunk_attn_bwd(const BwdArgs& a, hipStream_t stream);
+
+// The allocation-free backward keeps its row statistics (2 * B * H * Nq
+// floats) in a static device array of this many floats (32 MiB) per device.
+constexpr int64_t kBwdScratchFloats = FASTVR_BWD_NOALLOC_MAX_FLOATS;
+// Device address of the current device's array (looked up once per device).
+hipError_t bwd_scratch(float** out);
 
 hipError_t launch_one_step(const void* z_lq, const void* v, void* z_hat, int64_t n, float sigma, bool out_bf16,
                            hipStream_t stream);

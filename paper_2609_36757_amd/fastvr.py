@@ -19,7 +19,8 @@ ERR_CAPACITY = 3
 ERR_HIP = 4
 
 EXPORTED = ("fastvr_chunk_attn_fwd", "fastvr_chunk_attn_fwd_ex", "fastvr_kv_cache_append",
-            "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_one_step_update",
+            "fastvr_chunk_attn_ring_step", "fastvr_chunk_attn_bwd", "fastvr_chunk_attn_bwd_noalloc",
+            "fastvr_one_step_update",
             "fastvr_tile_axis", "fastvr_tile_gather", "fastvr_tile_blend", "fastvr_tile_blend_update",
             "fastvr_status_string", "fastvr_last_error", "fastvr_abi_version")
 
@@ -57,6 +58,9 @@ def load() -> ctypes.CDLL:
     lib.fastvr_chunk_attn_bwd.restype = ctypes.c_int
     lib.fastvr_chunk_attn_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64,
                                           _i64, _i64, _i64, _i64, ctypes.c_float, _vp]
+    lib.fastvr_chunk_attn_bwd_noalloc.restype = ctypes.c_int
+    lib.fastvr_chunk_attn_bwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64,
+                                                  _i64, _i64, _i64, _i64, _i64, ctypes.c_float, _vp]
     lib.fastvr_one_step_update.restype = ctypes.c_int
     lib.fastvr_one_step_update.argtypes = [_vp, _vp, _vp, _i64, ctypes.c_float, ctypes.c_int32, _vp]
     lib.fastvr_tile_axis.restype = ctypes.c_int
@@ -122,6 +126,12 @@ def bwd_raw(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chun
             window_chunks, scale, stream=0) -> int:
     return load().fastvr_chunk_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, row_stats, B, H, Nq, Nkv, d, chunk_len,
                                         q_chunk_offset, window_chunks, scale, stream)
+
+
+def bwd_noalloc_raw(q, k, v, o, lse, dout, dq, dk, dv, B, H, Nq, Nkv, d, chunk_len, q_chunk_offset, window_chunks,
+                    scale, stream=0) -> int:
+    return load().fastvr_chunk_attn_bwd_noalloc(q, k, v, o, lse, dout, dq, dk, dv, B, H, Nq, Nkv, d, chunk_len,
+                                                q_chunk_offset, window_chunks, scale, stream)
 
 
 def one_step_raw(z_lq, v, z_hat, n, sigma, out_bf16, stream=0) -> int:
@@ -295,6 +305,34 @@ def chunk_attn_bwd(q, k, v, o, lse, dout, *, chunk_len: int, q_chunk_offset: int
     _check(bwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), dout.data_ptr(),
                    dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), row_stats.data_ptr(), B, H, Nq, Nkv, d, chunk_len,
                    q_chunk_offset, window_chunks, scale, _stream_handle(stream)))
+    return dq, dk, dv
+
+
+def chunk_attn_bwd_noalloc(q, k, v, o, lse, dout, dq, dk, dv, *, chunk_len: int, q_chunk_offset: int = 0,
+                           window_chunks: int = -1, scale: float | None = None, stream=None):
+    """chunk_attn_bwd for callers that cannot allocate: the caller passes the
+    outputs dq, dk, dv (fp32, contiguous, shapes as in chunk_attn_bwd) and the
+    row statistics go to the library's static per-device workspace, so neither
+    the library nor this binding allocates.  Calls that overlap in time on one
+    device race on that workspace."""
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bfloat16 GPU tensor")
+    B, Nq, H, d = q.shape
+    Nkv = k.shape[1]
+    if k.shape != (B, Nkv, H, d) or v.shape != k.shape or dout.shape != q.shape:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)} "
+                         f"dout {tuple(dout.shape)}")
+    for name, t, shape in (("o", o, (B, Nq, H, d)), ("lse", lse, (B, H, Nq)), ("dq", dq, (B, Nq, H, d)),
+                           ("dk", dk, (B, Nkv, H, d)), ("dv", dv, (B, Nkv, H, d))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 {list(shape)} tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    _check(bwd_noalloc_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), dout.data_ptr(),
+                           dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nkv, d, chunk_len, q_chunk_offset,
+                           window_chunks, scale, _stream_handle(stream)))
     return dq, dk, dv
 
 

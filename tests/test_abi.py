@@ -39,7 +39,7 @@ def test_header_symbols_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.fastvr_abi_version() == 6
+    assert lib.fastvr_abi_version() == 7
     assert lib.fastvr_status_string(0) == b"FASTVR_OK"
     assert lib.fastvr_status_string(1) == b"FASTVR_ERR_INVALID_ARGUMENT"
     assert lib.fastvr_status_string(2) == b"FASTVR_ERR_UNSUPPORTED"
@@ -246,6 +246,36 @@ def test_bwd_empty_is_ok(lib, kw):
     assert _bwd(**kw) == fastvr.OK
 
 
+def _bwd_na(**kw):
+    a = dict(BWD_GOOD)
+    a.update(kw)
+    return fastvr.bwd_noalloc_raw(a["q"], a["k"], a["v"], a["o"], a["lse"], a["dout"], a["dq"], a["dk"], a["dv"],
+                                  a["B"], a["H"], a["Nq"], a["Nkv"], a["d"], a["chunk_len"], a["q_chunk_offset"],
+                                  a["window_chunks"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(q=None), fastvr.ERR_INVALID_ARGUMENT, "q is NULL"),
+    (dict(lse=None), fastvr.ERR_INVALID_ARGUMENT, "lse is NULL"),
+    (dict(lse=LSE + 2), fastvr.ERR_INVALID_ARGUMENT, "lse is not 4-byte aligned"),
+    (dict(dk=DK + 8), fastvr.ERR_INVALID_ARGUMENT, "aligned"),
+    (dict(d=96), fastvr.ERR_UNSUPPORTED, "head_dim"),
+    (dict(Nkv=63), fastvr.ERR_INVALID_ARGUMENT, "would not see its own key"),
+    (dict(dq=Q + 64), fastvr.ERR_INVALID_ARGUMENT, "dq overlaps q"),
+    (dict(dv=LSE), fastvr.ERR_INVALID_ARGUMENT, "dv overlaps lse"),
+    # 2 * B * H * Nq above the 8 Mi floats of the static workspace
+    (dict(H=64, Nq=65537, Nkv=65537), fastvr.ERR_UNSUPPORTED, "at most 8388608"),
+])
+def test_bwd_noalloc_rejects(lib, kw, status, needle):
+    assert _bwd_na(**kw) == status
+    assert needle in fastvr.last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(B=0), dict(H=0), dict(Nq=0, Nkv=0)])
+def test_bwd_noalloc_empty_is_ok(lib, kw):
+    assert _bwd_na(**kw) == fastvr.OK
+
+
 OS_GOOD = dict(z=Z, v=VEL, out=ZH, n=1000, sigma=0.5, out_bf16=0)
 
 
@@ -368,6 +398,8 @@ def test_valid_calls_reach_the_launcher(lib):
         lambda: _bwd(),
         lambda: _bwd(d=128, Nq=16, Nkv=64, q_chunk_offset=3, window_chunks=1),
         lambda: _bwd(Nq=0, q=None, dout=None, o=None, dq=None, lse=None, rs=None),
+        lambda: _bwd_na(),
+        lambda: _bwd_na(H=64, Nq=65536, Nkv=65536, d=128),
         lambda: _os(),
         lambda: _os(out=Z, out_bf16=1),
         lambda: _tg(),
