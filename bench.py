@@ -89,6 +89,102 @@ def cpu_baseline(w, q, k, v, budget_rows: int, seed: int = 0):
             "wall_s_full_call_extrapolated": round(dt * total / flops, 1)}
 
 
+class ClockSampler:
+    """Samples the GPU's graphics clock, activity and socket power from amdsmi's
+    GPU metrics in a background thread.  The firmware refreshes these metrics
+    about once a second, so the sampler runs over a window of about two seconds
+    of repeated (untimed) steps after the timed ones, and keeps the refreshes
+    taken under load (graphics activity >= 50%).  The chip runs below its
+    2.4 GHz peak clock under a power limit, so this is the clock a fraction of
+    the nominal MFMA peak has to be read against.  Reports nothing (with the
+    reason) when amdsmi is missing or the GPU is not found."""
+
+    def __init__(self, torch, period_s: float = 0.05):
+        self.period_s = period_s
+        self.handle = None
+        self.reason = None
+        self.samples = []
+        self._stop = None
+        self._thread = None
+        try:
+            import amdsmi
+            self.amdsmi = amdsmi
+            amdsmi.amdsmi_init()
+            handles = amdsmi.amdsmi_get_processor_handles()
+            bus = torch.cuda.get_device_properties(0).pci_bus_id
+            for h in handles:
+                try:
+                    if int(amdsmi.amdsmi_get_gpu_device_bdf(h).split(":")[1], 16) == bus:
+                        self.handle = h
+                        break
+                except Exception:
+                    continue
+            if self.handle is None and len(handles) == 1:
+                self.handle = handles[0]
+            if self.handle is None:
+                self.reason = f"no amdsmi device matches PCI bus {bus:#x} among {len(handles)}"
+        except Exception as e:  # amdsmi missing or not usable here
+            self.reason = f"amdsmi unavailable: {type(e).__name__}: {e}"[:200]
+
+    def _one(self):
+        m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.handle)
+        num = lambda x: float(x) if isinstance(x, (int, float)) and x >= 0 else None
+        per_xcc = m.get("current_gfxclks")
+        clk = None
+        if isinstance(per_xcc, (list, tuple)):
+            vals = [num(x) for x in per_xcc if num(x)]
+            clk = sum(vals) / len(vals) if vals else None
+        if clk is None:
+            clk = num(m.get("current_gfxclk"))
+        power = num(m.get("current_socket_power"))
+        if power is None:
+            power = num(m.get("average_socket_power"))
+        return clk, num(m.get("average_gfx_activity")), power
+
+    def _run(self):
+        import time as _t
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._one())
+            except Exception as e:
+                self.reason = f"metrics read failed: {type(e).__name__}: {e}"[:200]
+                return
+            _t.sleep(self.period_s)
+
+    def measure(self, torch, step, seconds: float = 2.0):
+        """Run step() repeatedly for about `seconds` while sampling; summary dict."""
+        import threading
+        import time as _t
+        if self.handle is None:
+            return {"source": None, "note": self.reason}
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        self._thread.start()
+        t0 = _t.perf_counter()
+        n = 0
+        while _t.perf_counter() - t0 < seconds:
+            for _ in range(5):
+                step()
+            torch.cuda.synchronize()
+            n += 5
+        self._stop.set()
+        self._thread.join(timeout=5)
+        loaded = []
+        for smp in self.samples:  # one entry per firmware refresh, taken under load
+            if smp[0] and smp[1] is not None and smp[1] >= 50 and (not loaded or smp != loaded[-1]):
+                loaded.append(smp)
+        if not loaded:
+            return {"source": None, "note": self.reason or "no metrics refresh under load during the window"}
+        mean = lambda xs: round(sum(xs) / len(xs), 1) if xs else None
+        clk = [c for c, _, _ in loaded]
+        pw = [p for _, _, p in loaded if p is not None]
+        return {"source": "amdsmi GPU metrics (current graphics clock, mean over the 8 XCDs), firmware refreshes "
+                          f"under load during {n} further untimed steps after the timed ones",
+                "refreshes": len(loaded), "gfxclk_mhz_mean": mean(clk), "gfxclk_mhz_min": min(clk),
+                "gfxclk_mhz_max": max(clk), "socket_power_w_mean": mean(pw),
+                "bf16_peak_at_mean_clock_tflops": round(PEAK_BF16_TFLOPS * mean(clk) / 2400.0, 1)}
+
+
 def _time_ms(torch, cur, fn, reps: int, warm: int = 2) -> float:
     """Average ms of fn() over reps calls, HIP events on the launch stream."""
     for _ in range(warm):
@@ -362,6 +458,7 @@ def main():
     end.record(cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    clock_info = ClockSampler(torch).measure(torch, step)
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
     per_full = sorted(e[0].elapsed_time(e[1]) for e in events)
@@ -408,6 +505,7 @@ def main():
         "roofline": {"kernel": "chunk_attn_fwd_kernel<128>", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic},
+        "clock": clock_info,
         "wall_s_timed": round(wall, 3),
     }
     if not args.no_extra:

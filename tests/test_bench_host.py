@@ -53,3 +53,31 @@ def test_source_hash_tracks_the_file(tmp_path, monkeypatch):
     src.write_text("kernel B\n")
     assert bench.kernel_source_hash() != h1
     assert len(h1) == 16 and all(c in "0123456789abcdef" for c in h1)
+
+
+def test_clock_summary_keeps_refreshes_under_load():
+    """bench.py's clock sampler reports only firmware refreshes taken under load
+    (activity >= 50%), one entry per distinct refresh, mean over the XCDs."""
+    import itertools
+    import types
+
+    import bench
+
+    seq = itertools.cycle([
+        {"current_gfxclks": [900, 900], "average_gfx_activity": 3, "current_socket_power": 280},
+        {"current_gfxclks": [1700, 1800], "average_gfx_activity": 100, "current_socket_power": 1390},
+        {"current_gfxclks": [1700, 1800], "average_gfx_activity": 100, "current_socket_power": 1390},
+        {"current_gfxclks": [1600, 1600], "average_gfx_activity": 99, "current_socket_power": 1400},
+    ])
+    fake_smi = types.SimpleNamespace(amdsmi_get_gpu_metrics_info=lambda h: next(seq))
+    fake_torch = types.SimpleNamespace(cuda=types.SimpleNamespace(synchronize=lambda: None))
+    cs = bench.ClockSampler.__new__(bench.ClockSampler)
+    cs.period_s, cs.handle, cs.reason, cs.samples, cs.amdsmi = 0.001, object(), None, [], fake_smi
+    cs._stop = cs._thread = None
+    r = cs.measure(fake_torch, lambda: None, seconds=0.05)
+    assert r["source"] is not None and r["refreshes"] >= 2
+    assert r["gfxclk_mhz_min"] == 1600 and r["gfxclk_mhz_max"] == 1750
+    assert 1600 <= r["gfxclk_mhz_mean"] <= 1750
+    cs2 = bench.ClockSampler.__new__(bench.ClockSampler)
+    cs2.handle, cs2.reason = None, "amdsmi unavailable"
+    assert cs2.measure(fake_torch, lambda: None)["source"] is None
