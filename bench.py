@@ -17,6 +17,7 @@ parallel calls with cold caches (``other_workloads``), then the fp64 oracle
 baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
+                      [--no-cpu-baseline] [--no-clock]
 """
 from __future__ import annotations
 
@@ -369,6 +370,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="1080p", choices=["1080p", "480p", "wide_sw", "tiny"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clock", action="store_true", help="skip the clock window after the timed steps")
     ap.add_argument("--cpu-rows", type=int, default=2560)
     ap.add_argument("--no-extra", action="store_true", help="skip the 480p / wide_sw / ring-step / backward timings")
     ap.add_argument("--bwd-only", action="store_true",
@@ -458,7 +460,7 @@ def main():
     end.record(cur)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    clock_info = ClockSampler(torch).measure(torch, step)
+    clock_info = {"source": None, "note": "--no-clock"} if args.no_clock else ClockSampler(torch).measure(torch, step)
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
     per_full = sorted(e[0].elapsed_time(e[1]) for e in events)

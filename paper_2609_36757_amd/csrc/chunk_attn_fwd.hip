@@ -162,7 +162,13 @@ __device__ __forceinline__ int item_of_block(const Params& p, int i) {
   return i;
 }
 
-template <int D, bool NEG, bool RING>
+// SPLIT: the matrix-core slot takes only each lane's row maximum of the fresh
+// scores; the exchange between the halves, the running maximum and s * c - m
+// move into the following vector-ALU slot (fused with the exp2).  Same
+// arithmetic either way (outputs are bit-identical).  The per-CU list kernel
+// uses it: it moves work out of the matrix-core slot, which helps the short
+// items of those calls, and it keeps that kernel within its registers.
+template <int D, bool NEG, bool RING, bool SPLIT = false>
 struct Attn {
   static constexpr int kChunks = D / 8;                        // 16-byte chunks per key row
   static constexpr int kStage = kBK * D;                       // bf16 elements per stage (K or V)
@@ -195,6 +201,7 @@ struct Attn {
   u32x4 pf[kKG];
   float m_run, l_run;
   float alpha;  // rescale factor of the tile whose statistics were taken last
+  float pmax;   // this lane's maximum of the fresh scores (before the exchange between halves)
 
   // XOR applied to the 16-byte chunk index of K row r: 16 consecutive rows read
   // the same logical chunk from 16 distinct bank groups
@@ -419,13 +426,51 @@ struct Attn {
       }
   }
 
-  // The rest of the online softmax once row_stats has run: P = exp2(t) rounded
-  // to bf16 fragments, l = l * alpha + rowsum(P), O *= alpha.
-  __device__ __forceinline__ void softmax_rest() {
+  // First half of the statistics of unmasked fresh scores: this lane's maximum
+  // (or minimum for a negative scale) only, with no dependency chain, so that
+  // it interleaves freely with MFMAs.
+  __device__ __forceinline__ void row_max_partial() {
+    constexpr float kInf = __builtin_inff();
+    float part[4] = {NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf, NEG ? kInf : -kInf};
 #pragma unroll
     for (int mb = 0; mb < kKB; ++mb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(s[mb][v]);
+      for (int v = 0; v < 16; ++v) {
+        float& pm = part[v & 3];
+        pm = NEG ? __builtin_fminf(pm, s[mb][v]) : __builtin_fmaxf(pm, s[mb][v]);
+      }
+    pmax = NEG ? __builtin_fminf(__builtin_fminf(part[0], part[1]), __builtin_fminf(part[2], part[3]))
+               : __builtin_fmaxf(__builtin_fmaxf(part[0], part[1]), __builtin_fmaxf(part[2], part[3]));
+  }
+
+  // Second half: the exchange between the halves, the running maximum and
+  // alpha, then P = exp2(s * c - m) in one pass.  Same arithmetic as row_stats
+  // followed by the exp2 of softmax_rest.
+  __device__ __forceinline__ void row_max_finish_exp() {
+    float other;
+    const float mine = swap_halves(pmax, &other);
+    const float mx = NEG ? __builtin_fminf(mine, other) : __builtin_fmaxf(mine, other);
+    const float m_new = __builtin_fmaxf(m_run, mx * c);
+    alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    const float nm = -m_new;
+#pragma unroll
+    for (int mb = 0; mb < kKB; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[mb][v], c, nm));
+  }
+
+  // The rest of the online softmax once row_stats has run: P = exp2(t) rounded
+  // to bf16 fragments, l = l * alpha + rowsum(P), O *= alpha.  With split
+  // statistics (EXP_DONE) the exp2 was already taken by row_max_finish_exp.
+  template <bool EXP_DONE = false>
+  __device__ __forceinline__ void softmax_rest() {
+    if (!EXP_DONE) {
+#pragma unroll
+      for (int mb = 0; mb < kKB; ++mb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[mb][v] = __builtin_amdgcn_exp2f(s[mb][v]);
+    }
     float ps[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
 #pragma unroll
     for (int mb = 0; mb < kKB; ++mb)
@@ -499,7 +544,12 @@ struct Attn {
         o[dm] = mfma32(__builtin_bit_cast(u32x4, vt[i]), pf[g], o[dm]);
       }
     }
-    if (STATS) row_stats<false>(kBK);
+    if (STATS) {
+      if (SPLIT)
+        row_max_partial();
+      else
+        row_stats<false>(kBK);
+    }
 #if FASTVR_SCHED
     if (PV) {
       if (!QK) __builtin_amdgcn_sched_group_barrier(SCHED_DS_READ, 2 * kAhead, 0);
@@ -514,6 +564,16 @@ struct Attn {
 #if FASTVR_PRIO
     __builtin_amdgcn_s_setprio(0);
 #endif
+  }
+
+  // The vector-ALU slot after a matrix-core slot that took the statistics.
+  __device__ __forceinline__ void softmax_after_stats() {
+    if (SPLIT) {
+      row_max_finish_exp();
+      softmax_rest<true>();
+    } else {
+      softmax_rest();
+    }
   }
 
   // Online softmax of the last tile (the only one that can be ragged): its
@@ -531,9 +591,9 @@ struct Attn {
 // One work item (a query tile of one batch, head and query chunk) from its
 // decode to its epilogue, run by the whole workgroup; smem is the workgroup's
 // LDS.  Waves without query rows leave before the epilogue.
-template <int D, bool NEG, bool RING>
+template <int D, bool NEG, bool RING, bool SPLIT = false>
 __device__ __forceinline__ void fwd_item(const Params& p, int vi, uint16_t* smem) {
-  using A = Attn<D, NEG, RING>;
+  using A = Attn<D, NEG, RING, SPLIT>;
   A a;
   a.ks = smem;
   a.vs = smem + kStages * A::kStage;
@@ -636,7 +696,7 @@ __device__ __forceinline__ void fwd_item(const Params& p, int vi, uint16_t* smem
       if (n == 1)
         a.softmax_last(last_valid);
       else
-        a.softmax_rest();
+        a.softmax_after_stats();
     } else {
       if (n == 1)
         a.template mfma_slot<true, false, false>(st_cur, 0);
@@ -657,14 +717,14 @@ __device__ __forceinline__ void fwd_item(const Params& p, int vi, uint16_t* smem
         if (group == 0)
           a.template mfma_slot<true, true, true>(st_cur, st_prev);
         else
-          a.softmax_rest();
+          a.softmax_after_stats();
       }
       barrier();
       // ---- slot 2j+1 ----
       if (v_issuer) a.load_v(j + 1, st_next);
       if (active) {
         if (group == 0)
-          a.softmax_rest();
+          a.softmax_after_stats();
         else
           a.template mfma_slot<true, true, true>(st_cur, st_prev);
       }
@@ -679,7 +739,7 @@ __device__ __forceinline__ void fwd_item(const Params& p, int vi, uint16_t* smem
       if (group == 0)
         a.template mfma_slot<true, true, false>(st_cur, st_prev);
       else
-        a.softmax_rest();
+        a.softmax_after_stats();
     }
     barrier();
     if (active) {
@@ -770,7 +830,7 @@ __global__ __launch_bounds__(kFwdThreads) void chunk_attn_fwd_list_kernel(const 
   __shared__ __attribute__((aligned(16))) uint16_t smem[Attn<D, NEG, false>::kLdsElems];
   const int g = blockIdx.x;
   for (int u = lst.start[g]; u < lst.start[g + 1]; ++u) {
-    fwd_item<D, NEG, false>(p, lst.item[u], smem);
+    fwd_item<D, NEG, false, true>(p, lst.item[u], smem);
     // every wave is done with the item's LDS stages before the next item's DMA
     barrier();
   }
