@@ -93,9 +93,11 @@ def cpu_baseline(w, q, k, v, budget_rows: int, seed: int = 0):
 class ClockSampler:
     """Samples the GPU's graphics clock, activity and socket power from amdsmi's
     GPU metrics in a background thread.  The firmware refreshes these metrics
-    about once a second, so the sampler runs over a window of about two seconds
-    of repeated (untimed) steps after the timed ones, and keeps the refreshes
-    taken under load (graphics activity >= 50%).  The chip runs below its
+    about once a second, so the sampler runs over a window of about three and a
+    half seconds of repeated (untimed) steps after the timed ones, and keeps the
+    refreshes taken under load (graphics activity >= 50%) after the first
+    second, whose refresh can still describe the ramp from the pause before the
+    window.  The chip runs below its
     2.4 GHz peak clock under a power limit, so this is the clock a fraction of
     the nominal MFMA peak has to be read against.  Reports nothing (with the
     reason) when amdsmi is missing or the GPU is not found."""
@@ -146,14 +148,15 @@ class ClockSampler:
         import time as _t
         while not self._stop.is_set():
             try:
-                self.samples.append(self._one())
+                self.samples.append((_t.perf_counter(),) + self._one())
             except Exception as e:
                 self.reason = f"metrics read failed: {type(e).__name__}: {e}"[:200]
                 return
             _t.sleep(self.period_s)
 
-    def measure(self, torch, step, seconds: float = 2.0):
-        """Run step() repeatedly for about `seconds` while sampling; summary dict."""
+    def measure(self, torch, step, seconds: float = 3.5, settle: float = 1.0):
+        """Run step() repeatedly for about `seconds` while sampling; summary dict
+        over the refreshes seen after the first `settle` seconds."""
         import threading
         import time as _t
         if self.handle is None:
@@ -170,17 +173,19 @@ class ClockSampler:
             n += 5
         self._stop.set()
         self._thread.join(timeout=5)
-        loaded = []
-        for smp in self.samples:  # one entry per firmware refresh, taken under load
-            if smp[0] and smp[1] is not None and smp[1] >= 50 and (not loaded or smp != loaded[-1]):
+        loaded, last = [], None
+        for t, *smp in self.samples:  # one entry per firmware refresh, taken under load
+            if smp != last and t - t0 >= settle and smp[0] and smp[1] is not None and smp[1] >= 50:
                 loaded.append(smp)
+            last = smp
         if not loaded:
             return {"source": None, "note": self.reason or "no metrics refresh under load during the window"}
         mean = lambda xs: round(sum(xs) / len(xs), 1) if xs else None
         clk = [c for c, _, _ in loaded]
         pw = [p for _, _, p in loaded if p is not None]
         return {"source": "amdsmi GPU metrics (current graphics clock, mean over the 8 XCDs), firmware refreshes "
-                          f"under load during {n} further untimed steps after the timed ones",
+                          f"under load during {n} further untimed steps after the timed ones (the first "
+                          f"{settle:g} s of them excluded)",
                 "refreshes": len(loaded), "gfxclk_mhz_mean": mean(clk), "gfxclk_mhz_min": min(clk),
                 "gfxclk_mhz_max": max(clk), "socket_power_w_mean": mean(pw),
                 "bf16_peak_at_mean_clock_tflops": round(PEAK_BF16_TFLOPS * mean(clk) / 2400.0, 1)}

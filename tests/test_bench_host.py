@@ -74,10 +74,14 @@ def test_clock_summary_keeps_refreshes_under_load():
     cs = bench.ClockSampler.__new__(bench.ClockSampler)
     cs.period_s, cs.handle, cs.reason, cs.samples, cs.amdsmi = 0.001, object(), None, [], fake_smi
     cs._stop = cs._thread = None
-    r = cs.measure(fake_torch, lambda: None, seconds=0.05)
+    r = cs.measure(fake_torch, lambda: None, seconds=0.05, settle=0.0)
     assert r["source"] is not None and r["refreshes"] >= 2
     assert r["gfxclk_mhz_min"] == 1600 and r["gfxclk_mhz_max"] == 1750
     assert 1600 <= r["gfxclk_mhz_mean"] <= 1750
+    # refreshes before the settle time are dropped (here: all of them)
+    cs.samples = []
+    r = cs.measure(fake_torch, lambda: None, seconds=0.02, settle=10.0)
+    assert r["source"] is None
     cs2 = bench.ClockSampler.__new__(bench.ClockSampler)
     cs2.handle, cs2.reason = None, "amdsmi unavailable"
     assert cs2.measure(fake_torch, lambda: None)["source"] is None
