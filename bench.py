@@ -17,7 +17,7 @@ parallel calls with cold caches (``other_workloads``), then the fp64 oracle
 baseline.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-extra] [--bwd-only]
-                      [--no-cpu-baseline] [--no-clock]
+                      [--no-cpu-baseline] [--no-clock] [--power-probe]
 """
 from __future__ import annotations
 
@@ -171,6 +171,7 @@ class ClockSampler:
                 step()
             torch.cuda.synchronize()
             n += 5
+        elapsed = _t.perf_counter() - t0
         self._stop.set()
         self._thread.join(timeout=5)
         loaded, last = [], None
@@ -188,7 +189,8 @@ class ClockSampler:
                           f"{settle:g} s of them excluded)",
                 "refreshes": len(loaded), "gfxclk_mhz_mean": mean(clk), "gfxclk_mhz_min": min(clk),
                 "gfxclk_mhz_max": max(clk), "socket_power_w_mean": mean(pw),
-                "bf16_peak_at_mean_clock_tflops": round(PEAK_BF16_TFLOPS * mean(clk) / 2400.0, 1)}
+                "bf16_peak_at_mean_clock_tflops": round(PEAK_BF16_TFLOPS * mean(clk) / 2400.0, 1),
+                "window_steps": n, "window_s": round(elapsed, 3)}
 
 
 def _time_ms(torch, cur, fn, reps: int, warm: int = 2) -> float:
@@ -368,6 +370,53 @@ def other_workloads(torch, fastvr, metrics, dev, cur, qd, kd, vd, w1080):
     return res
 
 
+def power_probe(torch, fastvr, dev):
+    """Clock and socket power under four loads, each run back to back for 3.5 s
+    (the first second excluded): a bf16 GEMM 8192^3 through torch.matmul
+    (hipBLASLt; a reference load of the same MFMA type), the 1080p and 480p
+    parallel forward calls, and the backward of the 1080p call.  Shows which
+    loads reach the board's power ceiling and at what clock."""
+    from paper_2609_36757_amd import metrics
+    from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence, randn_bf16
+    out = {}
+    sampler = lambda: ClockSampler(torch)
+
+    def entry(r, flop):
+        if r.get("source") is None:
+            return r
+        r = dict(r)
+        r.pop("source", None)
+        r["tflops"] = round(flop * r["window_steps"] / r["window_s"] / 1e12, 1)
+        return r
+
+    a = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    out["gemm_bf16_8192"] = entry(sampler().measure(torch, lambda: a @ a), 2 * 8192 ** 3)
+    del a
+    w = WORKLOADS["1080p"]
+    q, k, v = (t.to(dev) for t in make_sequence(w))
+    o = torch.empty((w.B, w.n_tokens, w.H, w.d), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.H, w.n_tokens), dtype=torch.float32, device=dev)
+    fwd = lambda: fastvr.chunk_attn(q, k, v, chunk_len=w.chunk_len, window_chunks=w.window_chunks, scale=w.scale,
+                                    out=o, lse=lse)
+    f1080 = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
+    out["fwd_1080p"] = entry(sampler().measure(torch, fwd), f1080)
+    g = torch.Generator().manual_seed(w.seed + 3000)
+    dout = randn_bf16((w.B, w.n_tokens, w.H, w.d), g).to(dev)
+    dq = torch.empty_like(o)
+    dk, dv = torch.empty_like(o), torch.empty_like(o)
+    rs = torch.empty((w.B, w.H, 2, w.n_tokens), dtype=torch.float32, device=dev)
+    bwd = lambda: fastvr.chunk_attn_bwd(q, k, v, o, lse, dout, chunk_len=w.chunk_len, window_chunks=w.window_chunks,
+                                        scale=w.scale, dq=dq, dk=dk, dv=dv, row_stats=rs)
+    out["bwd_1080p_effective"] = entry(sampler().measure(torch, bwd), 2.5 * f1080)
+    del q, k, v, o, lse, dout, dq, dk, dv, rs
+    w4 = WORKLOADS["480p"]
+    q, k, v = (t.to(dev) for t in make_sequence(w4))
+    f480 = metrics.effective_flops(w4.B, w4.H, w4.d, w4.n_tokens, w4.n_tokens, w4.chunk_len, 0, w4.window_chunks)
+    out["fwd_480p"] = entry(sampler().measure(torch, lambda: fastvr.chunk_attn(
+        q, k, v, chunk_len=w4.chunk_len, window_chunks=w4.window_chunks, scale=w4.scale)), f480)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -378,6 +427,8 @@ def main():
     ap.add_argument("--no-clock", action="store_true", help="skip the clock window after the timed steps")
     ap.add_argument("--cpu-rows", type=int, default=2560)
     ap.add_argument("--no-extra", action="store_true", help="skip the 480p / wide_sw / ring-step / backward timings")
+    ap.add_argument("--power-probe", action="store_true",
+                    help="only report the clock and socket power under a GEMM and the attention calls")
     ap.add_argument("--bwd-only", action="store_true",
                     help="time only the backward of the 1080p call (--steps calls) and print its figures")
     args = ap.parse_args()
@@ -399,6 +450,10 @@ def main():
     w = WORKLOADS[args.workload]
     q, k, v = make_sequence(w)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    if args.power_probe:
+        print("[bench] clock and power under a GEMM, the 1080p and 480p forward and the backward", flush=True)
+        print(json.dumps({"power_probe": power_probe(torch, fastvr, dev)}), flush=True)
+        return
     if args.bwd_only:
         w = WORKLOADS["1080p"]
         if args.workload != "1080p":
