@@ -82,12 +82,22 @@ def cpu_baseline(w, q, k, v, budget_rows: int, seed: int = 0):
         vis += hi - lo
     flops = 4 * w.d * w.B * w.H * vis
     total = metrics.effective_flops(w.B, w.H, w.d, w.n_tokens, w.n_tokens, w.chunk_len, 0, w.window_chunks)
+    # The oracle forms every (query, key) score of a row and then masks, so its
+    # time scales with the dense work B * H * Nq * Nkv * d of a call; the other
+    # configurations are extrapolated from the sample's rate in that measure.
+    from paper_2609_36757_amd.workloads import WORKLOADS
+    dense_rate = w.B * w.H * budget_rows * w.n_tokens * w.d / dt
+    per_cfg = {}
+    for name, c in WORKLOADS.items():
+        nq = c.chunk_len if c.stream_chunk is not None else c.n_tokens
+        per_cfg[name] = round(c.B * c.H * nq * c.n_tokens * c.d / dense_rate, 2)
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{budget_rows} seeded random query rows of the parallel 1080p call, all {w.H} heads, "
                       f"{dt:.1f} s wall, fp64 NumPy/BLAS ({threads} BLAS threads, 1 process), host "
                       f"os.cpu_count()={os.cpu_count()}",
             "wall_s_sample": round(dt, 2),
-            "wall_s_full_call_extrapolated": round(dt * total / flops, 1)}
+            "wall_s_full_call_extrapolated": round(dt * total / flops, 1),
+            "wall_s_per_config_extrapolated": per_cfg}
 
 
 class ClockSampler:
@@ -97,10 +107,10 @@ class ClockSampler:
     half seconds of repeated (untimed) steps after the timed ones, and keeps the
     refreshes taken under load (graphics activity >= 50%) after the first
     second, whose refresh can still describe the ramp from the pause before the
-    window.  The chip runs below its
-    2.4 GHz peak clock under a power limit, so this is the clock a fraction of
-    the nominal MFMA peak has to be read against.  Reports nothing (with the
-    reason) when amdsmi is missing or the GPU is not found."""
+    window.  Under load the firmware holds the chip below its 2.4 GHz peak
+    clock, so this is the clock a fraction of the nominal MFMA peak has to be
+    read against.  Reports nothing (with the reason) when amdsmi is missing or
+    the GPU is not found."""
 
     def __init__(self, torch, period_s: float = 0.05):
         self.period_s = period_s

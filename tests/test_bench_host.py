@@ -85,3 +85,23 @@ def test_clock_summary_keeps_refreshes_under_load():
     cs2 = bench.ClockSampler.__new__(bench.ClockSampler)
     cs2.handle, cs2.reason = None, "amdsmi unavailable"
     assert cs2.measure(fake_torch, lambda: None)["source"] is None
+
+
+def test_cpu_baseline_reports_every_configuration():
+    """bench.py's oracle baseline on a small sample of the tiny workload: the
+    rate, the sample's wall time and the per-configuration extrapolation, which
+    scales with the dense work B * H * Nq * Nkv * d of each configuration."""
+    import bench
+    from paper_2609_36757_amd.workloads import WORKLOADS, make_sequence
+
+    w = WORKLOADS["tiny"]
+    q, k, v = make_sequence(w)
+    r = bench.cpu_baseline(w, q, k, v, budget_rows=64, seed=1)
+    assert r["kind"] == "oracle" and r["value"] > 0 and r["wall_s_sample"] >= 0
+    per = r["wall_s_per_config_extrapolated"]
+    assert set(per) == set(WORKLOADS)
+    dense = {n: c.B * c.H * (c.chunk_len if c.stream_chunk is not None else c.n_tokens) * c.n_tokens * c.d
+             for n, c in WORKLOADS.items()}
+    # ratios of the extrapolated times follow the dense work (up to the rounding to 0.01 s)
+    assert per["wide_sw"] > per["1080p"] > per["1080p_stream"] > per["480p"] >= per["tiny"]
+    assert abs(per["wide_sw"] / per["1080p"] - dense["wide_sw"] / dense["1080p"]) < 0.05 * dense["wide_sw"] / dense["1080p"]
