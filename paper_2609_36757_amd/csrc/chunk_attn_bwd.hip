@@ -57,6 +57,7 @@ using namespace dev;
 #define FASTVR_PRIO 1  // raise the wave priority during matrix-core slots
 #endif
 
+
 constexpr int kTile = 64;  // rows per staged tile: keys (dQ) or queries (dK/dV)
 constexpr int kStages = 3;
 constexpr int kDqWaves = kBwdDqThreads / 64;    // 8
@@ -361,7 +362,13 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
       }
       u32x4 dsf[2];
       pack_bf16_half(s, dsf);
-      // dQ^T += K^T dS^T over keys 32 mb .. 32 mb + 31
+      // dQ^T += K^T dS^T over keys 32 mb .. 32 mb + 31, at a raised priority:
+      // the other wave of the SIMD is then most often in its S / dP MFMAs or
+      // its exp2, and these transposed-read MFMAs go first (the whole
+      // backward 0.5% faster; raising the S / dP MFMAs as well is not)
+#if FASTVR_PRIO
+      __builtin_amdgcn_s_setprio(1);
+#endif
       if (FASTVR_DQ_AHEAD > 0) {
         constexpr int kN = 2 * (D / 32);
         constexpr int kA = FASTVR_DQ_AHEAD < kN ? FASTVR_DQ_AHEAD : kN;
@@ -388,6 +395,9 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
 #pragma unroll
           for (int dm = 0; dm < D / 32; ++dm) acc[dm] = mfma32(rd.tr(kst, 2 * mb + gg, dm), dsf[gg], acc[dm]);
       }
+#if FASTVR_PRIO
+      __builtin_amdgcn_s_setprio(0);
+#endif
     }
     wait_vmcnt<2 * Dma::kPer>();
     barrier();
