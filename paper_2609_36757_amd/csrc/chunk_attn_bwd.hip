@@ -440,7 +440,7 @@ __global__ __launch_bounds__(kBwdDqThreads) void chunk_attn_bwd_dq_kernel(const 
 // Time is cut into slots separated by workgroup barriers, and the two groups
 // swap between a matrix-core slot and a vector-ALU slot every slot:
 //   slot 2t:   A  S(t) and dV += dO^T(t-1) P(t-1)       B  dS(t-1); DMA of Q(t+2), row stats(t+2)
-//   slot 2t+1: A  P(t) (exp2), P(t) to LDS; DMA dO(t+2)  B  dP(t) - D and dK += Q^T(t-1) dS(t-1)
+//   slot 2t+1: A  DMA dO(t+2); P(t) (exp2), P(t) to LDS  B  dP(t) - D and dK += Q^T(t-1) dS(t-1)
 // A tile is read from slot 2t to slot 2t+3, so the LDS holds four stages.
 // The dP accumulator starts from -D (read from the row statistics), so
 // dP - D comes out of the MFMAs.
@@ -733,6 +733,9 @@ __global__ __launch_bounds__(kBwdDkvThreads) void chunk_attn_bwd_dkv_kernel(cons
   __builtin_amdgcn_s_waitcnt(0x0F70);
   barrier();
 
+  // In its vector-ALU slot group B issues the DMA of Q(t + 2) after forming
+  // dS, group A that of dO(t + 2) before forming P: 1% faster than the other
+  // three orders (one process, alternated turns, identical gradients).
   const int n = n_tiles;
   for (int t = 0; t < n; ++t) {
     // ---- slot 2t ----
@@ -742,14 +745,14 @@ __global__ __launch_bounds__(kBwdDkvThreads) void chunk_attn_bwd_dkv_kernel(cons
       else
         a.template a_mfma<true, true>(t);
     } else {
-      load_b(t + 2);
       if (t > 0) a.b_valu();
+      load_b(t + 2);
     }
     barrier();
     // ---- slot 2t+1 ----
     if (group == 0) {
-      a.a_valu(t);
       load_a(t + 2);
+      a.a_valu(t);
       wait_vmcnt<Dma::kPer>();
     } else {
       if (t == 0)
