@@ -17,8 +17,11 @@
  *
  * Conventions shared by every entry point
  *  - All tensor pointers are DEVICE pointers owned by the caller.  The library
- *    allocates nothing, keeps no pointer after returning, has no global mutable
- *    state besides a thread-local error string, and is re-entrant.
+ *    allocates nothing and keeps no pointer after returning.  Its only global
+ *    state is a thread-local error string, caches (guarded, safe for concurrent
+ *    callers) of each device's CU count and of the last few work plans of the
+ *    forward, and the per-device static array of fastvr_chunk_attn_bwd_noalloc.
+ *    Every entry point except that one is re-entrant.
  *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.  Calls
  *    return after enqueueing; work is ordered on `stream`.  Faults during
  *    execution surface at the caller's next synchronisation of that stream.
