@@ -751,3 +751,125 @@ def test_tile_pins_catch_a_missing_normalisation(monkeypatch):
         for tx, ax in enumerate(oy):
             acc[ay:ay + L, ax:ax + L] += np.outer(w, w) * t[0, ty * len(oy) + tx, 0, :, :, 0]
     assert np.abs(acc - x[0, 0, :, :, 0]).max() > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# more plausible mistakes planted in the oracle, each run against an existing
+# pin, which must then fail
+# ---------------------------------------------------------------------------
+
+def _m_attention_default_scale():
+    """attention applying 1/sqrt(d) whatever scale it is given."""
+    orig = oc.attention
+
+    def attn(q, k, v, chunk_len, q_chunk_offset=0, window_chunks=-1, scale=None, rows=None, block=512):
+        return orig(q, k, v, chunk_len, q_chunk_offset, window_chunks, None, rows, block)
+    return "attention", attn
+
+
+def _m_attention_lse_log2():
+    """attention returning the log-sum-exp in base 2."""
+    orig = oc.attention
+
+    def attn(*a, **kw):
+        o, lse = orig(*a, **kw)
+        return o, lse / math.log(2.0)
+    return "attention", attn
+
+
+def _m_bwd(kind):
+    """attention_bwd with the row term's sign flipped, or dK without the scale."""
+    def bwd(q, k, v, do, chunk_len, q_chunk_offset=0, window_chunks=-1, scale=None, block=512, rows=None):
+        B, nq, H, d = q.shape
+        nkv = k.shape[1]
+        scale = 1.0 / math.sqrt(d) if scale is None else scale
+        vis = oc.visibility_mask(nq, nkv, chunk_len, q_chunk_offset, window_chunks)
+        dq, dk, dv = np.zeros(q.shape), np.zeros(k.shape), np.zeros(v.shape)
+        for b in range(B):
+            for h in range(H):
+                qh, kh, vh, doh = q[b, :, h], k[b, :, h], v[b, :, h], do[b, :, h]
+                s = np.where(vis, scale * (qh @ kh.T), -np.inf)
+                p = np.exp(s - s.max(axis=1, keepdims=True))
+                p /= p.sum(axis=1, keepdims=True)
+                dp = doh @ vh.T
+                row = (p * dp).sum(axis=1, keepdims=True)
+                ds = p * (dp + row) if kind == "row_term_sign" else p * (dp - row)
+                dq[b, :, h] = scale * (ds @ kh)
+                dk[b, :, h] = (ds.T @ qh) if kind == "dk_without_scale" else scale * (ds.T @ qh)
+                dv[b, :, h] = p.T @ doh
+        return dq, dk, dv
+    return "attention_bwd", bwd
+
+
+def _m_bwd_keys_without_row_term():
+    """attention_bwd_keys that ignores D (dS = P dP)."""
+    orig = oc.attention_bwd_keys
+
+    def keys_fn(q, k, v, do, keys, lse, delta, *a, **kw):
+        return orig(q, k, v, do, keys, lse, np.zeros(np.shape(delta)), *a, **kw)
+    return "attention_bwd_keys", keys_fn
+
+
+def _m_ring_forgets_the_new_chunk():
+    """ring_step that attends correctly but never stores the new chunk."""
+    orig = oc.ring_step
+
+    def step(k_ring, v_ring, *a, **kw):
+        o, lse, _, _ = orig(k_ring.copy(), v_ring.copy(), *a, **kw)
+        return o, lse, k_ring, v_ring
+    return "ring_step", step
+
+
+def _m_append_off_by_one():
+    """kv_cache_append writing one row past cache_len."""
+    orig = oc.kv_cache_append
+
+    def append(k_cache, v_cache, k_new, v_new, cache_len):
+        return orig(k_cache, v_cache, k_new, v_new, cache_len + 1)
+    return "kv_cache_append", append
+
+
+def _m_one_tile_too_few():
+    """tile_axis placing one tile fewer than needed (still evenly spaced)."""
+    import oracle.tiles as ot
+    orig = ot.tile_axis
+
+    def axis(size, tile, overlap):
+        origins, L = orig(size, tile, overlap)
+        n = len(origins) - 1
+        if n < 2:
+            return origins, L
+        return [(j * (size - L) + (n - 1) // 2) // (n - 1) for j in range(n)], L
+    return "tile_axis", axis
+
+
+def _m_weights_without_clamp():
+    """Feather weights min(i + 1, L - i) without the cap at the overlap."""
+    def weights(L, overlap):
+        i = np.arange(L)
+        return np.minimum(i + 1, L - i).astype(np.float64)
+    return "axis_weights", weights
+
+
+PLANTED = [
+    ("attention_default_scale", _m_attention_default_scale, lambda: test_oracle_matches_brute_force(1, 2, 2, 7, 0, 14)),
+    ("attention_lse_log2", _m_attention_lse_log2, lambda: check_hand_example(oracle.attention)),
+    ("bwd_row_term_sign", lambda: _m_bwd("row_term_sign"), lambda: test_bwd_matches_autograd(-1, 0, 40, 40, 8)),
+    ("bwd_dk_without_scale", lambda: _m_bwd("dk_without_scale"), lambda: test_bwd_matches_autograd(1, 0, 37, 37, 6)),
+    ("bwd_keys_without_row_term", _m_bwd_keys_without_row_term,
+     lambda: test_bwd_keys_matches_autograd(-1, 0, 40, 40, 8)),
+    ("ring_forgets_new_chunk", _m_ring_forgets_the_new_chunk, lambda: test_ring_holds_the_last_w_plus_one_chunks(1)),
+    ("append_off_by_one", _m_append_off_by_one, test_kv_append_oracle),
+    ("one_tile_too_few", _m_one_tile_too_few, lambda: test_tile_axis_properties(1000, 64, 32)),
+    ("weights_without_clamp", _m_weights_without_clamp, test_tile_closed_forms),
+]
+
+
+@pytest.mark.parametrize("name,mutant,pin", PLANTED, ids=[p[0] for p in PLANTED])
+def test_pins_catch_more_planted_mistakes(name, mutant, pin, monkeypatch):
+    """The pin passes with the oracle as it is (checked by its own test) and
+    fails once the planted mistake replaces the function."""
+    attr, fn = mutant()
+    monkeypatch.setattr(oracle, attr, fn)
+    with pytest.raises(AssertionError):
+        pin()
