@@ -68,6 +68,47 @@ def test_noalloc_at_the_1080p_shape(dev):
     _both(dev, q, k, v, do, o, lse, w.chunk_len, 0, w.window_chunks)
 
 
+def test_noalloc_in_a_hip_graph(dev):
+    """Captured in a HIP graph (what callers that cannot allocate need it for)
+    and replayed three times.  Before each replay an eager call of another shape
+    rewrites the static array and the outputs are poisoned: every replay must
+    give the eager result bit for bit."""
+    B, H, d, nq, nkv, L, off, W, seed = 1, 2, 128, 600, 600, 200, 0, -1, 63
+    print(f"\n[gpu case] bwd_noalloc in a HIP graph B={B} H={H} d={d} N={nq} L={L}", flush=True)
+    q, k, v, do, o, lse = _case(dev, B, H, d, nq, nkv, L, off, W, seed)
+    dq = torch.empty((B, nq, H, d), dtype=torch.float32, device=dev)
+    dk, dv = torch.empty((B, nkv, H, d), dtype=torch.float32, device=dev), torch.empty((B, nkv, H, d), device=dev)
+    run = lambda: fastvr.chunk_attn_bwd_noalloc(q, k, v, o, lse, do, dq, dk, dv, chunk_len=L, q_chunk_offset=off,
+                                                window_chunks=W)
+    # another shape, run eagerly between replays (same static array)
+    q2, k2, v2, do2, o2, lse2 = _case(dev, 1, 3, 64, 300, 500, 100, 2, 1, seed + 5)
+    dq2 = torch.empty((1, 300, 3, 64), dtype=torch.float32, device=dev)
+    dk2, dv2 = torch.empty((1, 500, 3, 64), device=dev), torch.empty((1, 500, 3, 64), device=dev)
+    other = lambda: fastvr.chunk_attn_bwd_noalloc(q2, k2, v2, o2, lse2, do2, dq2, dk2, dv2, chunk_len=100,
+                                                  q_chunk_offset=2, window_chunks=1)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()   # eager first: also looks up the array's address outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (dq, dk, dv)]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (dq, dk, dv):
+            t.fill_(float("nan"))
+        other()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, a, b in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32)), (rep, name)
+    print("[parity] bwd_noalloc graph replays x3 bit-identical to eager", flush=True)
+
+
 def test_noalloc_rejects_workspace_above_the_limit(dev):
     """2 * B * H * Nq above FASTVR_BWD_NOALLOC_MAX_FLOATS is refused on the host
     (no kernel runs; the tensors are never read)."""
