@@ -104,6 +104,7 @@ BWD_CASES = [
     ("negative_scale_d64", 1, 2, 64, 300, 300, 70, 0, 1, -0.3, 19),
     ("odd_L257", 1, 1, 128, 600, 600, 257, 0, -1, None, 20),
     ("multi_tile_chunks", 1, 1, 128, 1500, 1500, 700, 0, -1, None, 21),
+    ("negative_scale_d128_stream", 1, 2, 128, 200, 600, 200, 2, 1, -0.08, 22),
 ]
 
 

@@ -42,24 +42,28 @@ RING_CASES = [
     ("w7_L24", 1, 1, 128, 24 * 10, 24, 7, 107),
     ("w1_L96_one_tile_per_chunk", 1, 2, 128, 96 * 4 + 50, 96, 1, 108),
     ("w2_L192_d64", 1, 2, 64, 192 * 4 + 10, 192, 2, 109),
+    # negative scale: the ring kernels that track the running minimum (optional 9th field: scale)
+    ("w1_L100_negative_scale", 1, 2, 128, 100 * 4 + 37, 100, 1, 110, -0.06),
+    ("w2_L72_d64_negative_scale", 2, 2, 64, 72 * 5 + 8, 72, 2, 111, -0.2),
 ]
 
 
 @pytest.mark.parametrize("case", RING_CASES, ids=[c[0] for c in RING_CASES])
 def test_ring_stream_equals_parallel(dev, case):
-    name, B, H, d, N, L, W, seed = case
-    _announce(f"ring {name} B={B} H={H} d={d} N={N} L={L} W={W}")
+    name, B, H, d, N, L, W, seed, *opt = case
+    scale = opt[0] if opt else default_scale(d)
+    _announce(f"ring {name} B={B} H={H} d={d} N={N} L={L} W={W} scale={scale}")
     q, k, v = make_qkv(B, N, N, H, d, seed)
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
-    full_o, full_l = fastvr.chunk_attn(qd, kd, vd, chunk_len=L, window_chunks=W)
+    full_o, full_l = fastvr.chunk_attn(qd, kd, vd, chunk_len=L, window_chunks=W, scale=scale)
     ring_k = torch.full((B, (W + 1) * L, H, d), float("nan"), dtype=torch.bfloat16, device=dev)
     ring_v = torch.full_like(ring_k, float("nan"))
     n_chunks = -(-N // L)
-    scale = default_scale(d)
     for c in range(n_chunks):
         s = slice(c * L, min((c + 1) * L, N))
         o, lse = fastvr.chunk_attn_ring_step(qd[:, s].contiguous(), kd[:, s].contiguous(), vd[:, s].contiguous(),
-                                             ring_k, ring_v, chunk_len=L, chunk_index=c, window_chunks=W)
+                                             ring_k, ring_v, chunk_len=L, chunk_index=c, window_chunks=W,
+                                             scale=scale)
         torch.cuda.synchronize()
         assert torch.equal(o, full_o[:, s]), f"chunk {c}: output differs from the parallel call"
         assert torch.equal(lse, full_l[:, :, s]), f"chunk {c}: lse differs from the parallel call"
