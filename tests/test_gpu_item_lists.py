@@ -49,3 +49,23 @@ def test_item_lists_equal_plain_dispatch_and_oracle(dev, d, scale, window):
     o_ref, l_ref = run_oracle(q, k, v, L, 0, window, scale, rows=rows)
     compare(to_np(o[:, ridx]), to_np(lse[:, :, ridx]), o_ref, l_ref,
             label=f"item lists d={d} scale={scale:.4f} W={window} ({len(rows)} rows)")
+
+
+def test_item_lists_bf16_output_strided_and_no_lse(dev):
+    """The list kernel's other output forms: O as bf16 into a strided view (the
+    fp32 result rounded to nearest even, bit for bit, nothing written outside
+    the view) and no LSE pointer (O unchanged)."""
+    d, n = 128, L * N_CHUNKS
+    print(f"\n[gpu case] item lists, bf16 strided O and no LSE: B=1 H={H} d={d} N={n} L={L}", flush=True)
+    q, k, v = (t.to(dev) for t in make_qkv(1, n, n, H, d, seed=760))
+    o32, l32 = fastvr.chunk_attn(q, k, v, chunk_len=L)
+    big = torch.full((1, n + 9, H, d), float("nan"), dtype=torch.bfloat16, device=dev)
+    ob = big[:, 3:3 + n]
+    _, l16 = fastvr.chunk_attn(q, k, v, chunk_len=L, out=ob)
+    o_nl, none = fastvr.chunk_attn(q, k, v, chunk_len=L, return_lse=False)
+    torch.cuda.synchronize()
+    assert none is None
+    assert torch.equal(ob.view(torch.int16), o32.to(torch.bfloat16).view(torch.int16))
+    assert torch.isnan(big[:, :3].float()).all() and torch.isnan(big[:, 3 + n:].float()).all()
+    assert torch.equal(l16, l32)
+    assert torch.equal(o_nl, o32)
